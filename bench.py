@@ -1,0 +1,291 @@
+"""Benchmark of the Re-ttention hot path on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
+
+One step is one call of the fused sparse attention + statistical reshape
+(rt_attn_sparse_reshape: Eq.5, Eq.9 with the ramp, Eq.10 residual) over the
+workload's step-2 inputs, with rho and R cached by a caching step (full
+attention, sparse attention, cache build) on its step-1 inputs.  Inputs are
+resident in HBM before the timed region.  The other calls of the path (index
+build, full attention, sparse attention, cache build, unfused reshape) are timed
+separately and reported under "path".
+
+Prints ONE JSON line on stdout; progress goes to stderr.
+"""
+
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0  # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0      # MI355X HBM3E
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def host_csr(wl):
+    """Row counts of the workload's mask: the same closed forms the library uses
+    (counts only; the CSR itself is built on the GPU)."""
+    from paper_2505_22918_amd import synth
+
+    nb = wl.n_blk
+    if wl.kind == synth.PAT_LOCAL2D:
+        return np.full(nb, min(wl.keep, nb))
+    if wl.kind == synth.PAT_VIDEO3D:
+        ntb = -(-wl.n_text // wl.block)
+        cnt = np.full(nb, ntb + min(wl.keep, nb - ntb))
+        cnt[:ntb] = ntb
+        return cnt
+    m = synth.explicit_block_mask(nb, wl.seed)
+    return m.sum(axis=1)
+
+
+def kept_flops(wl, row_ptr, col_idx):
+    """4 * rows(qb) * cols(kb) * D summed over kept block pairs, times B*H."""
+    sizes = np.minimum(wl.block, wl.T - np.arange(wl.n_blk) * wl.block)
+    tot = 0
+    for qb in range(wl.n_blk):
+        cols = col_idx[row_ptr[qb]:row_ptr[qb + 1]]
+        tot += int(sizes[qb]) * int(sizes[cols].sum())
+    return 4.0 * tot * wl.D * wl.B * wl.H
+
+
+def fused_bytes(wl, stats=False):
+    """Compulsory HBM bytes of one fused call: Q, K, V, R read, O written (bf16),
+    rho read (fp32), plus m and l written when requested."""
+    n = wl.B * wl.H * wl.T
+    b = 2 * n * wl.D * 5 + 4 * n
+    if stats:
+        b += 8 * n
+    return float(b)
+
+
+def time_calls(fn, iters, stream):
+    """Average ms per call over `iters` back-to-back launches on `stream`."""
+    import torch
+
+    start = torch.cuda.Event(enable_timing=True)
+    end = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record(stream)
+    for _ in range(iters):
+        fn()
+    end.record(stream)
+    torch.cuda.synchronize()
+    return start.elapsed_time(end) / iters
+
+
+def cpu_baseline(wl, s2, rp, ci, rho, resid, budget_s=12.0):
+    """The oracle's sparse+reshape step on whole heads until ~budget_s of work."""
+    from oracle import attention as oa
+    from paper_2505_22918_amd import synth
+
+    try:
+        import threadpoolctl
+
+        blas_threads = max((i.get("num_threads", 1) for i in threadpoolctl.threadpool_info()), default=1)
+    except Exception:
+        blas_threads = None
+    f = lambda b: synth.bf16_bits_to_f32(b).astype(np.float64)
+    heads = [(b, h) for b in range(wl.B) for h in range(wl.H)]
+    done = 0
+    t_total = 0.0
+    for (b, h) in heads:
+        q = f(s2[0][b:b + 1, h:h + 1])
+        k = f(s2[1][b:b + 1, h:h + 1])
+        v = f(s2[2][b:b + 1, h:h + 1])
+        t0 = time.perf_counter()
+        o_s, _, _ = oa.sparse_attention(q, k, v, rp, ci, wl.block)
+        oa.reshape(o_s, rho[b:b + 1, h:h + 1], resid[b:b + 1, h:h + 1], 0.0)
+        t_total += time.perf_counter() - t0
+        done += 1
+        if t_total >= budget_s:
+            break
+    frac = done / len(heads)
+    return t_total, done, len(heads), frac, blas_threads
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="cogvideox_2b")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-path", action="store_true", help="skip timing the other calls of the path")
+    ap.add_argument("--cpu-budget", type=float, default=12.0)
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py runs on one GPU only: the attention path is sharded by heads with no "
+              "collective, and this build measures the one-GPU share (use --gpus 1).", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import paper_2505_22918_amd as rt
+    from paper_2505_22918_amd import _lib, synth
+
+    _lib.load()
+    wl = synth.WORKLOADS[args.workload]
+    dev = "cuda:0"
+    torch.cuda.set_device(0)
+    log(f"workload {wl.name}: B={wl.B} H={wl.H} T={wl.T} D={wl.D} block={wl.block}")
+
+    s1 = synth.make_qkv(wl, 1)
+    s2 = synth.make_qkv(wl, 2)
+    to_dev = lambda b: torch.from_numpy(np.ascontiguousarray(b).view(np.int16)).to(dev).view(torch.bfloat16)
+    kw = {k: v for k, v in wl.pattern_kwargs().items() if k != "kind"}
+    hm = synth.explicit_block_mask(wl.n_blk, wl.seed) if wl.kind == synth.PAT_EXPLICIT else None
+    if hm is not None:
+        mask = rt.build_index(wl.T, wl.block, wl.kind, device=dev, host_mask=hm)
+    else:
+        mask = rt.build_index(wl.T, wl.block, wl.kind, device=dev, **kw)
+    rp = mask.row_ptr.cpu().numpy()
+    ci = mask.col_idx.cpu().numpy()
+    flops = kept_flops(wl, rp, ci)
+    dense_flops = 4.0 * wl.B * wl.H * wl.T * wl.T * wl.D
+    density = mask.nnz / float(wl.n_blk ** 2)
+    log(f"mask nnz={mask.nnz} density={density:.4%} kept GFLOP={flops / 1e9:.2f}")
+
+    q1, k1, v1 = (to_dev(x) for x in s1)
+    q2, k2, v2 = (to_dev(x) for x in s2)
+    stream = torch.cuda.current_stream()
+
+    # caching step on step-1 inputs
+    of, mf, lf = rt.attn_full(q1, k1, v1, block=wl.block)
+    os_, ms, ls = rt.attn_sparse(q1, k1, v1, mask)
+    rho, resid = rt.cache_build(of, mf, lf, os_, ms, ls)
+    out = torch.empty_like(q2)
+    torch.cuda.synchronize()
+
+    fused = lambda: rt.attn_sparse_reshape(q2, k2, v2, mask, rho, resid, 0.0, out=out)
+    for _ in range(args.warmup):
+        fused()
+    torch.cuda.synchronize()
+    # timed region: exactly K steps between synchronisations
+    start = torch.cuda.Event(enable_timing=True)
+    end = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t_wall0 = time.perf_counter()
+    start.record(stream)
+    for _ in range(args.steps):
+        fused()
+    end.record(stream)
+    torch.cuda.synchronize()
+    t_wall = (time.perf_counter() - t_wall0) * 1e3 / args.steps
+    ms_call = start.elapsed_time(end) / args.steps
+    tflops = flops / (ms_call * 1e-3) / 1e12
+    nbytes = fused_bytes(wl)
+    gbs = nbytes / (ms_call * 1e-3) / 1e9
+    ai = flops / nbytes
+    ridge = PEAK_BF16_TFLOPS * 1e12 / (PEAK_HBM_GBS * 1e9)
+    log(f"fused sparse+reshape: {ms_call * 1e3:.1f} us/call, {tflops:.1f} TFLOP/s "
+        f"({tflops / PEAK_BF16_TFLOPS:.1%} of bf16 peak), {gbs:.0f} GB/s algorithmic")
+
+    path = {}
+    if not args.no_path:
+        t_dense = time_calls(lambda: rt.attn_full(q2, k2, v2, block=wl.block, stats=False, out=out), 3, stream)
+        t_sparse = time_calls(lambda: rt.attn_sparse(q2, k2, v2, mask, stats=True), 10, stream)
+        os2, _, _ = rt.attn_sparse(q2, k2, v2, mask)
+        t_apply = time_calls(lambda: rt.reshape_apply(os2, rho, resid, 0.0, out=out), 10, stream)
+        t_cache = time_calls(lambda: rt.cache_build(of, mf, lf, os_, ms, ls), 10, stream)
+        if hm is not None:
+            t_index = time_calls(lambda: rt.build_index(wl.T, wl.block, wl.kind, device=dev, host_mask=hm), 3,
+                                 stream)
+        else:
+            t_index = time_calls(lambda: rt.build_index(wl.T, wl.block, wl.kind, device=dev, **kw), 3, stream)
+        n = wl.B * wl.H * wl.T
+        ew_bytes = 2 * n * wl.D * 3 + 4 * n
+        cache_bytes = 2 * n * wl.D * 3 + 4 * n * 5
+        path = {
+            "index_build_ms": round(t_index, 4),
+            "attn_full_ms": round(t_dense, 4),
+            "attn_full_tflops": round(dense_flops / (t_dense * 1e-3) / 1e12, 2),
+            "attn_sparse_ms": round(t_sparse, 4),
+            "cache_build_ms": round(t_cache, 4),
+            "cache_build_gbs": round(cache_bytes / (t_cache * 1e-3) / 1e9, 1),
+            "reshape_apply_ms": round(t_apply, 4),
+            "reshape_apply_gbs": round(ew_bytes / (t_apply * 1e-3) / 1e9, 1),
+            "unfused_ms": round(t_sparse + t_apply, 4),
+            "speedup_vs_dense": round(t_dense / ms_call, 2),
+        }
+        log(f"path: {path}")
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        rho_h = rho.cpu().numpy().astype(np.float64)
+        resid_h = resid.float().cpu().numpy().astype(np.float64)
+        t_cpu, done, total, frac, blas = cpu_baseline(wl, s2, rp, ci, rho_h, resid_h, args.cpu_budget)
+        cores = len(os.sched_getaffinity(0))
+        cpu_tflops = flops * frac / t_cpu / 1e12
+        cpu = {
+            "value": cpu_tflops,
+            "unit": "TFLOP/s",
+            "cores": int(blas or cores),
+            "host_cores": cores,
+            "kind": "oracle",
+            "sample": f"{done} of {total} (batch, head) pairs, every query row; fp64 NumPy sparse "
+                      f"attention + reshape; {t_cpu:.1f} s",
+            "ms_per_call_extrapolated": t_cpu / frac * 1e3,
+        }
+        log(f"cpu oracle: {cpu}")
+
+    bound = "hbm" if ai < ridge else "mfma"
+    roof = {
+        "bound": bound,
+        "achieved": gbs if bound == "hbm" else tflops,
+        "peak": PEAK_HBM_GBS if bound == "hbm" else PEAK_BF16_TFLOPS,
+        "unit": "GB/s" if bound == "hbm" else "TFLOP/s",
+        "frac": (gbs / PEAK_HBM_GBS) if bound == "hbm" else (tflops / PEAK_BF16_TFLOPS),
+        "traffic": None,
+        "kernel": "attn_fwd<D,block,reshape=true>",
+        "algorithmic_bytes": nbytes,
+        "algorithmic_flops": flops,
+        "arith_intensity": ai,
+    }
+    rec = {
+        "metric": "sparse+reshape attention ms/call and kept-block TFLOP/s (% bf16 MFMA peak)",
+        "value": tflops,
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_call,
+        "ms_per_call": ms_call,
+        "host_ms_per_step": t_wall,
+        "mfma_frac": tflops / PEAK_BF16_TFLOPS,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {
+            "workload": wl.name,
+            "B": wl.B, "H": wl.H, "T": wl.T, "D": wl.D, "block": wl.block,
+            "nnz_blocks": int(mask.nnz), "density": density,
+            "kept_gflop": flops / 1e9, "dense_gflop": dense_flops / 1e9,
+            "parallelism": "single GPU",
+        },
+        "roofline": roof,
+        "cpu_baseline": cpu,
+        "path": path,
+    }
+    print(json.dumps(rec), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,172 @@
+/*
+ * rettention.h — C ABI of the MI355X (gfx950) Re-ttention attention library.
+ *
+ * Re-ttention (arXiv 2505.22918) runs block-sparse softmax attention at very
+ * high sparsity and corrects each query row with statistics cached at an
+ * earlier full-attention denoising step: the sparse softmax is scaled by the
+ * ratio rho of the sparse to the full softmax denominator (Eq.8, Eq.9) and the
+ * cached residual R of the masked tokens is added (Eq.10, App. A.3).
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ *  - Q, K, V, O and R are bf16 tensors [B, H, T, D], contiguous, row-major
+ *    (D fastest).  D is the real head width d_h; supported D: 64, 72.
+ *  - Scores are A^pre = Q K^T / sqrt(D) with the real D (Eq.2).
+ *  - Row statistics are fp32 [B, H, T]: row_max m = max_j A^pre_ij and
+ *    row_sum l = sum_j exp(A^pre_ij - m) over the keys the call attends to,
+ *    so l * exp(m) is the softmax denominator of Eq.4 (dense) or Eq.5 (sparse).
+ *  - rho is fp32 [B, H, T]; one value per batch element, head and query row.
+ *  - The block mask is a CSR over blocks of `block` tokens shared by every
+ *    (batch, head): block b covers tokens [b*block, min((b+1)*block, T)),
+ *    n_qblk = n_kblk = ceil(T / block).  row_ptr has n_qblk+1 entries, col_idx
+ *    lists the kept key blocks of each query block in ascending order.  A key
+ *    past T is never attended to.
+ *  - Tensor pointers marked "device" are device memory owned by the caller; the
+ *    library allocates nothing and keeps no state except a thread-local error
+ *    string.  Every call that takes `stream` (a hipStream_t passed as void*)
+ *    only enqueues work on it and returns; results are ready after the caller
+ *    synchronises that stream.
+ *  - Argument errors are found on the host before anything is enqueued, and
+ *    the call then returns a non-zero rt_status and enqueues nothing.  A launch
+ *    failure returns RT_EHIP.  rt_last_error() describes the last failure on
+ *    the calling thread.
+ *  - A call with B*H*T == 0 checks its arguments and enqueues nothing.
+ */
+#ifndef RETTENTION_H
+#define RETTENTION_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    RT_OK = 0,
+    RT_EINVAL = 1,       /* a null pointer, a negative or inconsistent size  */
+    RT_EUNSUPPORTED = 2, /* a head width or block size this build lacks      */
+    RT_ECAPACITY = 3,    /* an output buffer smaller than the result needs   */
+    RT_EHIP = 4          /* the HIP runtime refused a launch                 */
+} rt_status;
+
+/* Shape of Q, K, V, O, R: [B, H, T, D]. */
+typedef struct {
+    int32_t B, H, T, D;
+} rt_dims;
+
+/* A block CSR on the device, shared by all (batch, head).
+ * row_ptr [n_qblk + 1] and col_idx [nnz] are device int32 arrays.  The kernels
+ * clamp row_ptr entries to [0, nnz] and skip column indices outside
+ * [0, n_qblk), so a malformed CSR cannot make them read out of bounds; a query
+ * block with no kept key block is outside Eq.5 (empty denominator) and its
+ * rows come out as NaN. */
+typedef struct {
+    const int32_t* row_ptr;
+    const int32_t* col_idx;
+    int32_t block;  /* 32 or 64 */
+    int32_t n_qblk; /* must equal ceil(T / block) */
+    int32_t nnz;    /* entries in col_idx */
+} rt_bsr;
+
+/* Static mask patterns (Sec.3 static masks; App. A.4 local windows). */
+enum {
+    RT_PAT_EXPLICIT = 0, /* given 0/1 block matrix                              */
+    RT_PAT_LOCAL2D = 1,  /* image latent grid_h x grid_w, spatial window        */
+    RT_PAT_VIDEO3D = 2   /* n_text text tokens then frames x grid_h x grid_w    */
+};
+
+typedef struct {
+    int32_t kind;
+    const uint8_t* mask;      /* EXPLICIT, device: n_qblk x n_qblk row-major 0/1  */
+    const uint8_t* host_mask; /* EXPLICIT, host copy read by rt_index_size only  */
+    int32_t grid_h, grid_w;   /* LOCAL2D and VIDEO3D latent grid                 */
+    int32_t frames;           /* VIDEO3D latent frames                           */
+    int32_t n_text;           /* VIDEO3D leading text tokens                     */
+    int32_t keep;             /* LOCAL2D: key blocks kept per query block;
+                                 VIDEO3D: video key blocks kept per video query
+                                 block (text key blocks are always kept)         */
+} rt_pattern;
+
+/*
+ * Block-index rule (the paper names local windows, App. A.4, but no block
+ * rule).  A block's centroid is the mean latent position of its tokens; image
+ * token t sits at (t / grid_w, t % grid_w); video token n_text + v sits at
+ * (v / (grid_h*grid_w), (v / grid_w) % grid_h, v % grid_w).  Candidate key
+ * blocks are ranked by (squared centroid distance, |kb - qb|, kb) ascending and
+ * the first ones kept; each row is stored in ascending kb.  LOCAL2D keeps
+ * min(keep, n_qblk) blocks.  VIDEO3D: a block with any text token is a text
+ * block; text query blocks keep all text key blocks only; video query blocks
+ * keep all text key blocks plus the min(keep, #video blocks) highest-ranked
+ * video key blocks.  The result is exact (integer arithmetic) and unique.
+ */
+
+/* Host only.  Writes the exact number of CSR entries rt_index_build produces.
+ * EXPLICIT reads pattern->host_mask (host, n_qblk x n_qblk).  Needs T >= 1,
+ * block in {32, 64}, grid sizes matching T (LOCAL2D: grid_h*grid_w == T;
+ * VIDEO3D: n_text + frames*grid_h*grid_w == T), keep >= 1, n_qblk <= 4096. */
+rt_status rt_index_size(const rt_pattern* pattern, int32_t T, int32_t block, int32_t* nnz_out);
+
+/* Builds the CSR on the device: row_ptr [ceil(T/block)+1], col_idx [capacity].
+ * For LOCAL2D / VIDEO3D the size is known on the host and a capacity below it
+ * is RT_ECAPACITY.  EXPLICIT reads pattern->mask (device) and writes at most
+ * `capacity` entries; it returns RT_ECAPACITY when pattern->host_mask is given
+ * and needs more, otherwise the caller must size capacity to the mask. */
+rt_status rt_index_build(const rt_pattern* pattern, int32_t T, int32_t block, int32_t* row_ptr,
+                         int32_t* col_idx, int32_t capacity, void* stream);
+
+/* Dense attention with row statistics, Eq.1 with the Eq.4 denominator.
+ * q, k, v: device bf16 [B,H,T,D]; o: device bf16 [B,H,T,D] (written);
+ * row_max, row_sum: device fp32 [B,H,T] (written, either may be NULL).
+ * The query tiling uses `block` rows (32 or 64). */
+rt_status rt_attn_full(const void* q, const void* k, const void* v, rt_dims dims, int32_t block,
+                       void* o, float* row_max, float* row_sum, void* stream);
+
+/* Sparse attention over a block mask, Eq.5: each row's softmax runs over the
+ * tokens of its query block's kept key blocks only.  Same buffers as
+ * rt_attn_full; row statistics are over the kept keys. */
+rt_status rt_attn_sparse(const void* q, const void* k, const void* v, rt_dims dims,
+                         const rt_bsr* mask, void* o, float* row_max, float* row_sum,
+                         void* stream);
+
+/* Statistics cache at a caching (full-attention) step, Eq.8 and Eq.10:
+ *   rho = (l_sparse / l_full) * exp(m_sparse - m_full)      (Eq.8)
+ *   R   = O_full - rho * O_sparse                           (Eq.10)
+ * o_full, o_sparse: device bf16 [B,H,T,D]; m_*, l_*: device fp32 [B,H,T];
+ * rho: device fp32 [B,H,T] (written); resid: device bf16 [B,H,T,D] (written,
+ * rounded to nearest even). */
+rt_status rt_cache_build(const void* o_full, const float* m_full, const float* l_full,
+                         const void* o_sparse, const float* m_sparse, const float* l_sparse,
+                         rt_dims dims, float* rho, void* resid, void* stream);
+
+/* Fused sparse attention + statistical reshape, Eq.5 then Eq.9 with the ramp
+ * of Sec.4.2 and the residual of Eq.10:
+ *   O = min(1, rho + rho_delta) * SparseAttention(Q,K,V) + R
+ * rho_delta = lambda * (t - c) is the ramp accumulated since the caching step
+ * c (0 for no ramp).  rho: device fp32 [B,H,T]; resid: device bf16 [B,H,T,D];
+ * o: device bf16 [B,H,T,D] (written); row_max / row_sum: device fp32 [B,H,T],
+ * the sparse statistics of this step, or NULL to skip writing them. */
+rt_status rt_attn_sparse_reshape(const void* q, const void* k, const void* v, rt_dims dims,
+                                 const rt_bsr* mask, const float* rho, const void* resid,
+                                 float rho_delta, void* o, float* row_max, float* row_sum,
+                                 void* stream);
+
+/* The same reshape applied to an already computed sparse output (unfused):
+ *   O = min(1, rho + rho_delta) * o_sparse + R
+ * o_sparse, resid, o: device bf16 [B,H,T,D]; rho: device fp32 [B,H,T]. */
+rt_status rt_reshape_apply(const void* o_sparse, const float* rho, const void* resid,
+                           float rho_delta, rt_dims dims, void* o, void* stream);
+
+/* Static description of a status code. */
+const char* rt_status_str(rt_status status);
+
+/* The message of the last failing call on this thread ("" if none). */
+const char* rt_last_error(void);
+
+/* Library version, major*10000 + minor*100 + patch. */
+int32_t rt_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* RETTENTION_H */

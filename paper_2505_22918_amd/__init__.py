@@ -1,0 +1,267 @@
+"""Re-ttention sparse attention with statistical reshape on MI355X (gfx950).
+
+Python face of librettention.so.  Functions take torch CUDA tensors for device
+memory and launch on torch's current stream; all computation runs in the HIP
+library (the binding only marshals pointers and sizes).
+
+  build_index           block CSR of the static mask (Sec.3, App. A.4)
+  attn_full             dense attention with row statistics (Eq.1, Eq.4)
+  attn_sparse           sparse attention over the block mask (Eq.5)
+  cache_build           rho and residual at a caching step (Eq.8, Eq.10)
+  attn_sparse_reshape   fused sparse attention + reshape + residual (Eq.5, 9, 10)
+  reshape_apply         the reshape on a precomputed sparse output (Eq.9, 10)
+  StatCache             per-layer cache of rho and R with the step schedule of Sec.5
+"""
+
+from __future__ import annotations
+
+import ctypes
+from dataclasses import dataclass
+
+from . import _lib
+from .synth import PAT_EXPLICIT, PAT_LOCAL2D, PAT_VIDEO3D
+
+__all__ = [
+    "BlockMask",
+    "index_size",
+    "build_index",
+    "attn_full",
+    "attn_sparse",
+    "cache_build",
+    "attn_sparse_reshape",
+    "reshape_apply",
+    "StatCache",
+    "PAT_EXPLICIT",
+    "PAT_LOCAL2D",
+    "PAT_VIDEO3D",
+]
+
+
+def _torch():
+    import torch
+
+    return torch
+
+
+def _stream(t):
+    torch = _torch()
+    return ctypes.c_void_p(torch.cuda.current_stream(t.device).cuda_stream)
+
+
+def _ptr(t):
+    return ctypes.c_void_p(t.data_ptr()) if t is not None else ctypes.c_void_p(0)
+
+
+def _check_qkv(q, k, v):
+    torch = _torch()
+    for name, t in (("q", q), ("k", k), ("v", v)):
+        if not isinstance(t, torch.Tensor) or t.device.type != "cuda":
+            raise ValueError(f"{name} must be a CUDA tensor")
+        if t.dtype != torch.bfloat16 or t.dim() != 4 or not t.is_contiguous():
+            raise ValueError(f"{name} must be a contiguous bf16 [B,H,T,D] tensor")
+        if t.shape != q.shape or t.device != q.device:
+            raise ValueError("q, k, v must share shape and device")
+    B, H, T, D = q.shape
+    return _lib.RtDims(B, H, T, D)
+
+
+def _stat(t, shape, name):
+    torch = _torch()
+    if t.dtype != torch.float32 or tuple(t.shape) != tuple(shape) or not t.is_contiguous():
+        raise ValueError(f"{name} must be a contiguous fp32 tensor of shape {tuple(shape)}")
+    return t
+
+
+def _bf16(t, shape, name):
+    torch = _torch()
+    if t.dtype != torch.bfloat16 or tuple(t.shape) != tuple(shape) or not t.is_contiguous():
+        raise ValueError(f"{name} must be a contiguous bf16 tensor of shape {tuple(shape)}")
+    return t
+
+
+@dataclass
+class BlockMask:
+    """Block CSR on the device: row_ptr [n_qblk+1], col_idx [nnz] (int32)."""
+
+    row_ptr: object
+    col_idx: object
+    block: int
+    n_qblk: int
+    nnz: int
+
+    def c_struct(self):
+        return _lib.RtBsr(self.row_ptr.data_ptr(), self.col_idx.data_ptr(), self.block, self.n_qblk,
+                          self.nnz)
+
+    @classmethod
+    def from_csr(cls, row_ptr, col_idx, block, device="cuda"):
+        """Copies a host CSR (numpy / lists) to the device as-is."""
+        torch = _torch()
+        rp = torch.as_tensor(row_ptr, dtype=torch.int32).to(device).contiguous()
+        ci = torch.as_tensor(col_idx, dtype=torch.int32).to(device).contiguous()
+        return cls(rp, ci, int(block), int(rp.numel()) - 1, int(ci.numel()))
+
+
+def _pattern(kind, grid_h=0, grid_w=0, frames=0, n_text=0, keep=0, mask=None, host_mask=None):
+    p = _lib.RtPattern()
+    p.kind = int(kind)
+    p.mask = mask.data_ptr() if mask is not None else None
+    p.host_mask = host_mask.ctypes.data if host_mask is not None else None
+    p.grid_h, p.grid_w, p.frames, p.n_text, p.keep = int(grid_h), int(grid_w), int(frames), int(n_text), int(keep)
+    return p
+
+
+def index_size(T, block, kind, host_mask=None, **pat):
+    """Exact CSR entry count of a pattern (host only)."""
+    import numpy as np
+
+    lib = _lib.load()
+    hm = np.ascontiguousarray(host_mask, dtype=np.uint8) if host_mask is not None else None
+    p = _pattern(kind, host_mask=hm, **pat)
+    out = ctypes.c_int32(0)
+    _lib.check("rt_index_size", lib.rt_index_size(ctypes.byref(p), int(T), int(block), ctypes.byref(out)))
+    return int(out.value)
+
+
+def build_index(T, block, kind, device="cuda", host_mask=None, **pat) -> BlockMask:
+    """Builds the block CSR on the device with the library's index kernels."""
+    import numpy as np
+
+    torch = _torch()
+    lib = _lib.load()
+    n_blk = (int(T) + int(block) - 1) // int(block)
+    hm = None
+    dmask = None
+    if kind == PAT_EXPLICIT:
+        hm = np.ascontiguousarray(host_mask, dtype=np.uint8)
+        if hm.shape != (n_blk, n_blk):
+            raise ValueError(f"host_mask must be {n_blk}x{n_blk}")
+        dmask = torch.from_numpy(hm).to(device)
+    nnz = index_size(T, block, kind, host_mask=hm, **pat)
+    row_ptr = torch.empty(n_blk + 1, dtype=torch.int32, device=device)
+    col_idx = torch.empty(max(nnz, 1), dtype=torch.int32, device=device)
+    p = _pattern(kind, mask=dmask, host_mask=hm, **pat)
+    _lib.check("rt_index_build", lib.rt_index_build(ctypes.byref(p), int(T), int(block), _ptr(row_ptr),
+                                                    _ptr(col_idx), int(nnz), _stream(row_ptr)))
+    if dmask is not None:
+        # keep the mask alive until the build has run on the stream
+        torch.cuda.current_stream(row_ptr.device).synchronize()
+    return BlockMask(row_ptr, col_idx[:nnz] if nnz else col_idx[:0], int(block), n_blk, int(nnz))
+
+
+def attn_full(q, k, v, block=64, stats=True, out=None):
+    """Dense attention (Eq.1) with row statistics of the Eq.4 denominator."""
+    torch = _torch()
+    lib = _lib.load()
+    dims = _check_qkv(q, k, v)
+    o = out if out is not None else torch.empty_like(q)
+    m = l = None
+    if stats:
+        m = torch.empty(q.shape[:3], dtype=torch.float32, device=q.device)
+        l = torch.empty_like(m)
+    _lib.check("rt_attn_full", lib.rt_attn_full(_ptr(q), _ptr(k), _ptr(v), dims, int(block), _ptr(o),
+                                                _ptr(m), _ptr(l), _stream(q)))
+    return (o, m, l) if stats else o
+
+
+def attn_sparse(q, k, v, mask: BlockMask, stats=True, out=None):
+    """Sparse attention over the block mask (Eq.5) with row statistics."""
+    torch = _torch()
+    lib = _lib.load()
+    dims = _check_qkv(q, k, v)
+    o = out if out is not None else torch.empty_like(q)
+    m = l = None
+    if stats:
+        m = torch.empty(q.shape[:3], dtype=torch.float32, device=q.device)
+        l = torch.empty_like(m)
+    bsr = mask.c_struct()
+    _lib.check("rt_attn_sparse", lib.rt_attn_sparse(_ptr(q), _ptr(k), _ptr(v), dims, ctypes.byref(bsr),
+                                                    _ptr(o), _ptr(m), _ptr(l), _stream(q)))
+    return (o, m, l) if stats else o
+
+
+def cache_build(o_full, m_full, l_full, o_sparse, m_sparse, l_sparse):
+    """rho (Eq.8) and residual R (Eq.10) at a caching step."""
+    torch = _torch()
+    lib = _lib.load()
+    B, H, T, D = o_full.shape
+    _bf16(o_full, o_full.shape, "o_full")
+    _bf16(o_sparse, o_full.shape, "o_sparse")
+    for name, t in (("m_full", m_full), ("l_full", l_full), ("m_sparse", m_sparse), ("l_sparse", l_sparse)):
+        _stat(t, (B, H, T), name)
+    rho = torch.empty((B, H, T), dtype=torch.float32, device=o_full.device)
+    resid = torch.empty_like(o_full)
+    _lib.check("rt_cache_build", lib.rt_cache_build(_ptr(o_full), _ptr(m_full), _ptr(l_full), _ptr(o_sparse),
+                                                    _ptr(m_sparse), _ptr(l_sparse), _lib.RtDims(B, H, T, D),
+                                                    _ptr(rho), _ptr(resid), _stream(o_full)))
+    return rho, resid
+
+
+def attn_sparse_reshape(q, k, v, mask: BlockMask, rho, resid, rho_delta=0.0, stats=False, out=None):
+    """Fused Eq.5 + Eq.9 (ramped) + Eq.10: min(1, rho + delta) * SparseAttn + R."""
+    torch = _torch()
+    lib = _lib.load()
+    dims = _check_qkv(q, k, v)
+    _stat(rho, q.shape[:3], "rho")
+    _bf16(resid, q.shape, "resid")
+    o = out if out is not None else torch.empty_like(q)
+    m = l = None
+    if stats:
+        m = torch.empty(q.shape[:3], dtype=torch.float32, device=q.device)
+        l = torch.empty_like(m)
+    bsr = mask.c_struct()
+    _lib.check("rt_attn_sparse_reshape",
+               lib.rt_attn_sparse_reshape(_ptr(q), _ptr(k), _ptr(v), dims, ctypes.byref(bsr), _ptr(rho),
+                                          _ptr(resid), float(rho_delta), _ptr(o), _ptr(m), _ptr(l), _stream(q)))
+    return (o, m, l) if stats else o
+
+
+def reshape_apply(o_sparse, rho, resid, rho_delta=0.0, out=None):
+    """Unfused Eq.9 + Eq.10 on a sparse output: min(1, rho + delta) * o_sparse + R."""
+    torch = _torch()
+    lib = _lib.load()
+    B, H, T, D = o_sparse.shape
+    _bf16(o_sparse, o_sparse.shape, "o_sparse")
+    _bf16(resid, o_sparse.shape, "resid")
+    _stat(rho, (B, H, T), "rho")
+    o = out if out is not None else torch.empty_like(o_sparse)
+    _lib.check("rt_reshape_apply", lib.rt_reshape_apply(_ptr(o_sparse), _ptr(rho), _ptr(resid), float(rho_delta),
+                                                        _lib.RtDims(B, H, T, D), _ptr(o), _stream(o_sparse)))
+    return o
+
+
+class StatCache:
+    """Per-attention-layer cache of rho and R driven by the step schedule.
+
+    Sec.5: full attention for the first ``full_steps`` denoising steps, then
+    sparse attention with a full "caching" step every ``period`` steps that
+    refreshes rho (Eq.8) and R (Eq.10).  Between caching steps the cached rho is
+    ramped by ``lam`` per step (Sec.4.2), i.e. rho_delta = lam * (t - c).
+    """
+
+    def __init__(self, mask: BlockMask, full_steps=5, period=5, lam=0.0):
+        self.mask = mask
+        self.full_steps = int(full_steps)
+        self.period = int(period)
+        self.lam = float(lam)
+        self.rho = None
+        self.resid = None
+        self.cached_at = None
+
+    def is_caching_step(self, t):
+        """Steps 0 .. full_steps-1 are full; afterwards every period-th step,
+        counted from the last full step, is a full caching step."""
+        if t < self.full_steps:
+            return True
+        return self.period > 0 and (t - self.full_steps + 1) % self.period == 0
+
+    def attend(self, q, k, v, t):
+        """Attention output at denoising step t (full at caching steps)."""
+        if self.is_caching_step(t) or self.rho is None:
+            o_f, m_f, l_f = attn_full(q, k, v, block=self.mask.block)
+            o_s, m_s, l_s = attn_sparse(q, k, v, self.mask)
+            self.rho, self.resid = cache_build(o_f, m_f, l_f, o_s, m_s, l_s)
+            self.cached_at = t
+            return o_f
+        delta = self.lam * (t - self.cached_at)
+        return attn_sparse_reshape(q, k, v, self.mask, self.rho, self.resid, rho_delta=delta)

@@ -1,0 +1,58 @@
+// Internal launch interface between the C ABI (api.cpp) and the HIP kernels.
+// Arguments reaching these launchers have already been validated on the host.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace rt {
+
+struct AttnArgs {
+    const uint16_t* q;  // bf16 [B,H,T,D]
+    const uint16_t* k;
+    const uint16_t* v;
+    uint16_t* o;        // bf16 [B,H,T,D]
+    float* row_max;     // fp32 [B,H,T] or null
+    float* row_sum;     // fp32 [B,H,T] or null
+    const float* rho;   // reshape only: fp32 [B,H,T]
+    const uint16_t* resid;  // reshape only: bf16 [B,H,T,D]
+    float rho_delta;
+    const int32_t* row_ptr;  // sparse only
+    const int32_t* col_idx;
+    int32_t nnz;
+    int32_t T;
+    int32_t n_blk;      // ceil(T / block)
+    int32_t dense;      // 1: walk every key block, ignore the CSR
+    int32_t n_items;    // B*H*n_blk workgroups of real work
+    int32_t per_xcd;    // ceil(n_items / 8)
+    float scale_log2;   // log2(e) / sqrt(D)
+    float scale_nat;    // 1 / sqrt(D)
+};
+
+hipError_t launch_attention(const AttnArgs& a, int D, int block, bool reshape, hipStream_t stream);
+
+hipError_t launch_cache_build(const uint16_t* o_full, const float* m_full, const float* l_full,
+                              const uint16_t* o_sparse, const float* m_sparse,
+                              const float* l_sparse, int64_t rows, int D, float* rho,
+                              uint16_t* resid, hipStream_t stream);
+
+hipError_t launch_reshape_apply(const uint16_t* o_sparse, const float* rho, const uint16_t* resid,
+                                float rho_delta, int64_t rows, int D, uint16_t* o,
+                                hipStream_t stream);
+
+struct IndexArgs {
+    int32_t kind;
+    const uint8_t* mask;  // EXPLICIT, device
+    int32_t T, block, n_blk;
+    int32_t grid_h, grid_w, frames, n_text;
+    int32_t keep;
+    int32_t n_tblk;       // VIDEO3D text blocks
+    int64_t lcm;          // lcm of candidate block token counts
+    int32_t* row_ptr;
+    int32_t* col_idx;
+    int32_t capacity;
+};
+
+hipError_t launch_index_build(const IndexArgs& a, hipStream_t stream);
+
+}  // namespace rt
