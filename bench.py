@@ -127,6 +127,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-path", action="store_true", help="skip timing the other calls of the path")
     ap.add_argument("--cpu-budget", type=float, default=12.0)
+    ap.add_argument("--copy-mb", type=int, default=0,
+                    help="also run K plain device copies of this many MiB (HBM counter calibration)")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -195,6 +197,14 @@ def main():
     ridge = PEAK_BF16_TFLOPS * 1e12 / (PEAK_HBM_GBS * 1e9)
     log(f"fused sparse+reshape: {ms_call * 1e3:.1f} us/call, {tflops:.1f} TFLOP/s "
         f"({tflops / PEAK_BF16_TFLOPS:.1%} of bf16 peak), {gbs:.0f} GB/s algorithmic")
+
+    if args.copy_mb > 0:
+        n = args.copy_mb * (1 << 20) // 2
+        src = torch.empty(n, dtype=torch.bfloat16, device=dev).fill_(1.0)
+        dst = torch.empty_like(src)
+        t_copy = time_calls(lambda: dst.copy_(src), args.steps, stream)
+        log(f"copy {args.copy_mb} MiB: {t_copy * 1e3:.1f} us, {2 * n * 2 / (t_copy * 1e-3) / 1e9:.0f} GB/s")
+        del src, dst
 
     path = {}
     if not args.no_path:
