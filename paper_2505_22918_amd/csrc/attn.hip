@@ -159,7 +159,7 @@ void attn_fwd(AttnArgs a) {
     constexpr int RSLOT = BS * DC;           // 16-byte slots of the R tile
     constexpr int NDMA_R = (RSLOT + 63) / 64;
     constexpr int SMEM = 2 * STAGE + 256;    // two stages + slack for padded V^T reads
-    static_assert(RSLOT * 16 <= STAGE, "R tile fits a stage");
+    static_assert(RSLOT * 16 <= 2 * TILE, "Q / R tile fits two stages");
     static_assert(ROWB == 2 * D, "rows are unpadded");
 
     __shared__ __attribute__((aligned(1024))) unsigned char smem[SMEM];
@@ -235,6 +235,8 @@ void attn_fwd(AttnArgs a) {
     // longer rows read the rest with scalar loads.
     int cols = -1;
     if (!a.dense && lane < e_end - e_beg) cols = ((csr_ptr)a.col_idx)[e_beg + lane];
+    wait_vm<0>();
+    asm volatile("" : "+v"(cols));  // the load has landed; later reads need no wait
     const int n_chunk = (e_end - e_beg) * (BS / 32);
     auto chunk_base = [&](int i) -> int {
         const int j = i / (BS / 32), half = i - j * (BS / 32);
@@ -250,69 +252,92 @@ void attn_fwd(AttnArgs a) {
         return (kb >= 0 && kb < a.n_blk && base < T) ? base : -1;
     };
 
-    // DMA of the 32-key K and V chunks starting at key `base` into ring stage `st`;
-    // the buffers end at row T, so rows past it read as zeros.
-    auto issue = [&](int base, int st) {
+    // LDS map: K stages at [0, TILE) and [TILE, 2 TILE), V stages at [2 TILE, 3 TILE)
+    // and [3 TILE, 4 TILE).  Before the walk the Q tile sits in the V stages; after
+    // the last K chunk has been read the residual / output tile takes the K stages.
+    auto k_off = [&](int st) { return st * TILE; };
+    auto v_off = [&](int st) { return (2 + st) * TILE; };
+
+    // DMA of the 32-key chunk of `head` starting at key `base` to LDS byte offset
+    // `dst`; the buffer ends at row T, so rows past it read as zeros.  A chunk that
+    // holds no key (base < 0) is not loaded.
+    auto issue = [&](const uint16_t* head, const int (&off)[NDMA], int base, int dst) {
         if (base < 0) return;
         const int left = (T - base) * (D * 2);
         const int nrec = left < 32 * D * 2 ? left : 32 * D * 2;
-        const i32x4 kr = buffer_rsrc(Kh + (size_t)base * D, nrec);
-        const i32x4 vr = buffer_rsrc(Vh + (size_t)base * D, nrec);
+        const i32x4 rs = buffer_rsrc(head + (size_t)base * D, nrec);
 #pragma unroll
         for (int n = 0; n < NDMA; ++n) {
-            if (NSLOT % 64 == 0 || n * 64 + lane < NSLOT) dma16(lds0 + st * STAGE + n * 1024, kdma[n], kr);
-        }
-#pragma unroll
-        for (int n = 0; n < NDMA; ++n) {
-            if (NSLOT % 64 == 0 || n * 64 + lane < NSLOT)
-                dma16(lds0 + st * STAGE + TILE + n * 1024, vdma[n], vr);
+            if (NSLOT % 64 == 0 || n * 64 + lane < NSLOT) dma16(lds0 + dst + n * 1024, off[n], rs);
         }
     };
-    // DMA of the block's residual rows into ring stage `st`, same row layout and
-    // swizzle as K (rows past T read as zeros)
-    auto issue_r = [&](int st) {
+    // DMA of the block's BS rows of `tensor` (Q or R) to LDS byte offset `dst`, same
+    // row layout and swizzle as K (rows past T read as zeros)
+    auto issue_rows = [&](const uint16_t* tensor, int dst) {
         const int left = (T - row0) * (D * 2);
         const int nrec = left < BS * D * 2 ? left : BS * D * 2;
-        const i32x4 rr = buffer_rsrc(a.resid + head_off + (size_t)row0 * D, nrec);
+        const i32x4 rr = buffer_rsrc(tensor + head_off + (size_t)row0 * D, nrec);
 #pragma unroll
         for (int n = 0; n < NDMA_R; ++n) {
             const int slot = n * 64 + lane;
             const int r = slot / DC, s = slot - (slot / DC) * DC;
             if (RSLOT % 64 == 0 || slot < RSLOT)
-                dma16(lds0 + st * STAGE + n * 1024, r * (D * 2) + ((s ^ kswz<D>(r)) * 16), rr);
+                dma16(lds0 + dst + n * 1024, r * (D * 2) + ((s ^ kswz<D>(r)) * 16), rr);
         }
     };
 
-    // ---- prologue: first chunk's DMA, Q, rho in flight together --------------------
-    int cur = n_chunk > 0 ? chunk_base(0) : -1;
-    int nxt = n_chunk > 1 ? chunk_base(1) : -1;
-    issue(cur, 0);
+    // wait until at most n vector-memory operations (the ones just issued) are
+    // outstanding; waiting for fewer is always safe, so take the largest constant <= n
+    auto wait_le = [&](int n) {
+        if (n >= 2 * NDMA + NDMA_R) {
+            wait_vm<2 * NDMA + NDMA_R>();
+        } else if (n >= NDMA + NDMA_R) {
+            wait_vm<NDMA + NDMA_R>();
+        } else if (n >= 2 * NDMA) {
+            wait_vm<2 * NDMA>();
+        } else if (n >= NDMA_R) {
+            wait_vm<NDMA_R>();
+        } else if (n >= NDMA) {
+            wait_vm<NDMA>();
+        } else {
+            wait_vm<0>();
+        }
+    };
 
+    // ---- prologue ---------------------------------------------------------------------
     float rho_r[QT];
 #pragma unroll
     for (int qt = 0; qt < QT; ++qt) {
         const int row = row0 + qt * 32 + l32;
         rho_r[qt] = (RESHAPE && row < T) ? a.rho[(size_t)bh * T + row] : 0.f;
     }
-    // Q^T operands: lane holds query l32 of tile qt, head dims 16s + 8hi .. +7
+    const int c0 = n_chunk > 0 ? chunk_base(0) : -1;
+    int c1 = n_chunk > 1 ? chunk_base(1) : -1;
+    issue(Kh, kdma, c0, k_off(0));
+    issue_rows(a.q, v_off(0));
+    issue(Kh, kdma, c1, k_off(1));
+    if (c1 >= 0) {
+        wait_vm<NDMA>();  // K(0) and the Q tile have landed; K(1) may be in flight
+    } else {
+        wait_vm<0>();
+    }
+
+    // Q^T operands from the Q tile: lane holds query l32 of tile qt, head dims
+    // 16s + 8hi .. +7 (zero past D)
     bf16x8 qop[QT][DS];
 #pragma unroll
     for (int qt = 0; qt < QT; ++qt) {
-        int row = row0 + qt * 32 + l32;
-        row = row < T ? row : T - 1;
-        const uint16_t* qr = a.q + head_off + (size_t)row * D;
+        const int rl = qt * 32 + l32;
 #pragma unroll
         for (int s = 0; s < DS; ++s) {
-            const int d0 = 16 * s + 8 * hi;
-            if (d0 < D) {
-                qop[qt][s] = *reinterpret_cast<const bf16x8*>(qr + d0);
+            const int ch = 2 * s + hi;
+            if (ch < DC) {
+                qop[qt][s] = *(const lds_bf16x8*)(lds + v_off(0) + rl * ROWB + ((ch ^ kswz<D>(rl)) * 16));
             } else {
                 qop[qt][s] = bf16x8{};
             }
         }
     }
-    wait_vm<0>();  // chunk 0, Q, rho and the CSR window have landed
-    issue(nxt, 1);
 
     const float c2 = a.scale_log2;  // log2(e) / sqrt(D)
     f32x16 oacc[QT][DT];
@@ -326,91 +351,37 @@ void attn_fwd(AttnArgs a) {
         for (int dt = 0; dt < DT; ++dt) oacc[qt][dt] = f32x16{};
     }
 
-    // probabilities of one 32-key chunk against the running max: bf16 operand for
-    // P V and the fp32 row sum of the lane's 16 keys
-    auto probs = [&](const f32x16& sc, float mrun, bf16x8 (&pp)[2]) {
-        const float mc = mrun * c2;
-        float lsum = 0.f;
+    // S^T = K Q^T for the K chunk in stage `st`
+    auto qk = [&](int st, f32x16 (&sc)[QT]) {
+        const lds_u8* Ks = lds + k_off(st);
+        bf16x8 kop[DS];
 #pragma unroll
-        for (int ks = 0; ks < 2; ++ks) {
+        for (int s = 0; s < DS; ++s) kop[s] = *(const lds_bf16x8*)(Ks + k_rd[s]);
 #pragma unroll
-            for (int x = 0; x < 8; ++x) {
-                const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[8 * ks + x], c2, -mc));
-                lsum += p;
-                pp[ks][x] = (__bf16)p;
-            }
-        }
-        return lsum;
-    };
-    // row max of one chunk; lane holds keys 8j + 4hi + i for acc index 4j + i, the
-    // other 16 keys of its query sit in lane l ^ 32
-    auto chunk_max = [&](const f32x16& sc) {
-        float mx = fmaxf(fmaxf(sc[0], sc[1]), sc[2]);
-#pragma unroll
-        for (int x = 3; x < 15; x += 2) mx = fmaxf(fmaxf(mx, sc[x]), sc[x + 1]);
-        mx = fmaxf(mx, sc[15]);
-        return pair_max(mx);
-    };
-
-    int st = 0;     // ring stage of chunk cur
-    int r_st = -1;  // stage the residual tile was brought into
-    for (int i = 0; i < n_chunk; ++i) {
-        const lds_u8* Ks = lds + st * STAGE;
-        const lds_u8* Vs = Ks + TILE;
-
-        // S^T = K Q^T
-        f32x16 sacc[QT];
-#pragma unroll
-        for (int qt = 0; qt < QT; ++qt) sacc[qt] = f32x16{};
+        for (int qt = 0; qt < QT; ++qt) sc[qt] = f32x16{};
 #pragma unroll
         for (int s = 0; s < DS; ++s) {
-            const bf16x8 kop = *(const lds_bf16x8*)(Ks + k_rd[s]);
 #pragma unroll
             for (int qt = 0; qt < QT; ++qt)
-                sacc[qt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kop, qop[qt][s], sacc[qt], 0, 0, 0);
+                sc[qt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kop[s], qop[qt][s], sc[qt], 0, 0, 0);
         }
-        if (cur < 0 || cur + 32 > T) {  // keys past T, or a chunk holding no key
-#pragma unroll
-            for (int qt = 0; qt < QT; ++qt) {
-#pragma unroll
-                for (int x = 0; x < 16; ++x) {
-                    const int key = cur + 8 * (x >> 2) + 4 * hi + (x & 3);
-                    if (cur < 0 || key >= T) sacc[qt][x] = -INFINITY;
-                }
-            }
-        }
-
-        // softmax against the stale max; the rare overflow case takes the slow path
-        bf16x8 pop[QT][2];
-        float lsum[QT];
-        float mx[QT];
-        bool jump = false;
+    };
+    // keys past T, or a chunk holding no key, score -inf
+    auto mask = [&](int base, f32x16 (&sc)[QT]) {
+        if (base >= 0 && base + 32 <= T) return;
 #pragma unroll
         for (int qt = 0; qt < QT; ++qt) {
-            if (STATS) {
-                mx[qt] = chunk_max(sacc[qt]);
-                m_top[qt] = fmaxf(m_top[qt], mx[qt]);
-            }
-            lsum[qt] = probs(sacc[qt], m_run[qt], pop[qt]);
-            jump |= !(lsum[qt] < kJump);
-        }
-        if (__builtin_amdgcn_ballot_w64(jump)) {
 #pragma unroll
-            for (int qt = 0; qt < QT; ++qt) {
-                if (!STATS) mx[qt] = chunk_max(sacc[qt]);
-                const float mnew = fmaxf(m_run[qt], mx[qt]);
-                const float alpha = __builtin_amdgcn_exp2f((m_run[qt] - mnew) * c2);
-                l_run[qt] *= alpha;
-#pragma unroll
-                for (int dt = 0; dt < DT; ++dt) oacc[qt][dt] *= alpha;
-                m_run[qt] = mnew;
-                lsum[qt] = probs(sacc[qt], m_run[qt], pop[qt]);
+            for (int x = 0; x < 16; ++x) {
+                const int key = base + 8 * (x >> 2) + 4 * hi + (x & 3);
+                if (base < 0 || key >= T) sc[qt][x] = -INFINITY;
             }
         }
-#pragma unroll
-        for (int qt = 0; qt < QT; ++qt) l_run[qt] += lsum[qt];
-
-        // O^T += V^T P^T; the V^T operand is two transpose reads of 4 rows each
+    };
+    // O^T += V^T P^T for the V chunk in stage `st`; the V^T operand is two
+    // transpose reads of 4 rows each
+    auto pv = [&](int st, const bf16x8 (&pp)[QT][2]) {
+        const lds_u8* Vs = lds + v_off(st);
 #pragma unroll
         for (int dt = 0; dt < DT; ++dt) {
 #pragma unroll
@@ -421,37 +392,212 @@ void attn_fwd(AttnArgs a) {
                 const bf16x8 vv = __builtin_shufflevector(v0, v1, 0, 1, 2, 3, 4, 5, 6, 7);
 #pragma unroll
                 for (int qt = 0; qt < QT; ++qt)
-                    oacc[qt][dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vv, pop[qt][ks], oacc[qt][dt], 0, 0, 0);
+                    oacc[qt][dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vv, pp[qt][ks], oacc[qt][dt], 0, 0, 0);
             }
         }
-
-        // refill the stage just consumed: chunk i+2, or the residual tile once the
-        // chunk sequence is exhausted; then wait for chunk i+1
-        const bool more = i + 2 < n_chunk;
-        const int nx2 = more ? chunk_base(i + 2) : -1;
-        if (nx2 >= 0) {
-            issue(nx2, st);
-            wait_vm<2 * NDMA>();
-        } else if (RESHAPE && !more && r_st < 0) {
-            issue_r(st);
-            r_st = st;
-            wait_vm<NDMA_R>();
-        } else {
-            wait_vm<0>();
+    };
+    // probabilities of 4 scores against the running max: bf16 operand values and
+    // their fp32 sum
+    auto probs4 = [&](const f32x16& sc, int x0, float mc, bf16x8& pp, int y0) {
+        float acc = 0.f;
+#pragma unroll
+        for (int x = 0; x < 4; ++x) {
+            const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[x0 + x], c2, -mc));
+            acc += p;
+            pp[y0 + x] = (__bf16)p;
         }
-        cur = nxt;
-        nxt = nx2;
-        st ^= 1;
+        return acc;
+    };
+    // row max of one chunk; lane holds keys 8j + 4hi + i for acc index 4j + i, the
+    // other 16 keys of its query sit in lane l ^ 32
+    auto chunk_max = [&](const f32x16& sc) {
+        float mx = fmaxf(fmaxf(sc[0], sc[1]), sc[2]);
+#pragma unroll
+        for (int x = 3; x < 15; x += 2) mx = fmaxf(fmaxf(mx, sc[x]), sc[x + 1]);
+        mx = fmaxf(mx, sc[15]);
+        return pair_max(mx);
+    };
+    // softmax of chunk scores `sc` against the running max; the rare case of a
+    // probability reaching 2^64 rescales O and l and recomputes (all PV products
+    // issued so far are in oacc by then)
+    auto softmax_tail = [&](f32x16 (&sc)[QT], bf16x8 (&pp)[QT][2], float (&lsum)[QT], float (&mx)[QT]) {
+        bool jump = false;
+#pragma unroll
+        for (int qt = 0; qt < QT; ++qt) jump |= !(lsum[qt] < kJump);
+        if (__builtin_amdgcn_ballot_w64(jump)) {
+#pragma unroll
+            for (int qt = 0; qt < QT; ++qt) {
+                if (!STATS) mx[qt] = chunk_max(sc[qt]);
+                const float mnew = fmaxf(m_run[qt], mx[qt]);
+                const float alpha = __builtin_amdgcn_exp2f((m_run[qt] - mnew) * c2);
+                l_run[qt] *= alpha;
+#pragma unroll
+                for (int dt = 0; dt < DT; ++dt) oacc[qt][dt] *= alpha;
+                m_run[qt] = mnew;
+                const float mc = mnew * c2;
+                lsum[qt] = probs4(sc[qt], 0, mc, pp[qt][0], 0) + probs4(sc[qt], 4, mc, pp[qt][0], 4) +
+                           probs4(sc[qt], 8, mc, pp[qt][1], 0) + probs4(sc[qt], 12, mc, pp[qt][1], 4);
+            }
+        }
+#pragma unroll
+        for (int qt = 0; qt < QT; ++qt) l_run[qt] += lsum[qt];
+    };
+
+    // Software pipeline over chunks 0 .. n-1.  Step t issues the DMA of K(t+2) and
+    // V(t) (into the stages K(t) and V(t-2) have left), then runs S(t+1) = K Q^T and
+    // the P V product of chunk t-1 on the matrix cores, spread over the vector work
+    // of chunk t's softmax.  The residual / output tile replaces the K stages once
+    // the last K chunk has been read.
+    f32x16 s_cur[QT];
+    bf16x8 p_prev[QT][2];
+    int r_issued = 0;
+    if (n_chunk > 0) {
+        qk(0, s_cur);
+        mask(c0, s_cur);
     }
-    if (RESHAPE && r_st < 0) {  // a block with no kept key block
-        issue_r(0);
-        r_st = 0;
+    // step 0: as the later steps, without a P V product yet
+    {
+        const int c2n = n_chunk > 2 ? chunk_base(2) : -1;
+        issue(Kh, kdma, c2n, k_off(0));  // K(0) has been read
+        issue(Vh, vdma, c0, v_off(0));   // the Q tile has been read
+        int now = (c2n >= 0 ? NDMA : 0) + (c0 >= 0 ? NDMA : 0);
+        if (RESHAPE && n_chunk <= 1) {  // no K chunk left to read
+            issue_rows(a.resid, 0);
+            r_issued = 1;
+            now += NDMA_R;
+        }
+        wait_le(now);  // K(1)
+        if (n_chunk > 0) {
+            f32x16 s_nxt[QT];
+            float lsum[QT], mx[QT];
+            bf16x8 pp[QT][2];
+            if (n_chunk > 1) qk(1, s_nxt);
+#pragma unroll
+            for (int qt = 0; qt < QT; ++qt) {
+                if (STATS) {
+                    mx[qt] = chunk_max(s_cur[qt]);
+                    m_top[qt] = fmaxf(m_top[qt], mx[qt]);
+                }
+                const float mc = m_run[qt] * c2;
+                lsum[qt] = probs4(s_cur[qt], 0, mc, pp[qt][0], 0) + probs4(s_cur[qt], 4, mc, pp[qt][0], 4) +
+                           probs4(s_cur[qt], 8, mc, pp[qt][1], 0) + probs4(s_cur[qt], 12, mc, pp[qt][1], 4);
+            }
+            softmax_tail(s_cur, pp, lsum, mx);
+#pragma unroll
+            for (int qt = 0; qt < QT; ++qt) {
+                p_prev[qt][0] = pp[qt][0];
+                p_prev[qt][1] = pp[qt][1];
+            }
+            if (n_chunk > 1) {
+#pragma unroll
+                for (int qt = 0; qt < QT; ++qt) s_cur[qt] = s_nxt[qt];
+                mask(c1, s_cur);
+            }
+        }
+    }
+    // rolling window of chunk bases: b_t = base(t), b_t1 = base(t+1)
+    int b_t = n_chunk > 1 ? c1 : -1;
+    int b_t1 = n_chunk > 2 ? chunk_base(2) : -1;
+    for (int t = 1; t < n_chunk; ++t) {
+        const int kst = t & 1;  // stage of K(t) and V(t)
+        // refill: K(t+2) -> stage of K(t), V(t) -> stage of V(t-2); the residual
+        // tile takes the K stages once the last K chunk (t) was read in step t-1
+        const int cn2 = t + 2 < n_chunk ? chunk_base(t + 2) : -1;
+        const int ct = b_t;
+        issue(Kh, kdma, cn2, k_off(kst));
+        issue(Vh, vdma, ct, v_off(kst));
+        if (RESHAPE && t == n_chunk - 1) {
+            issue_rows(a.resid, 0);
+            r_issued = 1;
+        }
+        // K(t+1) and V(t-1) were issued one step earlier
+        wait_le((cn2 >= 0 ? NDMA : 0) + (ct >= 0 ? NDMA : 0) + ((RESHAPE && t == n_chunk - 1) ? NDMA_R : 0));
+
+        // interleaved block: S(t+1) and P V(t-1) on the matrix cores, softmax(t) on
+        // the vector unit (after the last chunk the S product reads a stale stage
+        // and is discarded)
+        f32x16 s_nxt[QT];
+        float lsum[QT], mx[QT];
+        bf16x8 pp[QT][2];
+        {
+            const lds_u8* Ks = lds + k_off(kst ^ 1);
+            const lds_u8* Vs = lds + v_off(kst ^ 1);
+            bf16x8 kop[DS];
+#pragma unroll
+            for (int s = 0; s < DS; ++s) kop[s] = *(const lds_bf16x8*)(Ks + k_rd[s]);
+            bf16x8 vop[DT][2];
+#pragma unroll
+            for (int dt = 0; dt < DT; ++dt) {
+#pragma unroll
+                for (int ks = 0; ks < 2; ++ks) {
+                    const bf16x4 v0 =
+                        __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(Vs + v_rd[dt] + 16 * ks * ROWB));
+                    const bf16x4 v1 =
+                        __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(Vs + v_rd[dt] + (16 * ks + 8) * ROWB));
+                    vop[dt][ks] = __builtin_shufflevector(v0, v1, 0, 1, 2, 3, 4, 5, 6, 7);
+                }
+            }
+#pragma unroll
+            for (int qt = 0; qt < QT; ++qt) {
+                s_nxt[qt] = f32x16{};
+                lsum[qt] = 0.f;
+            }
+            if (STATS) {
+#pragma unroll
+                for (int qt = 0; qt < QT; ++qt) {
+                    mx[qt] = chunk_max(s_cur[qt]);
+                    m_top[qt] = fmaxf(m_top[qt], mx[qt]);
+                }
+            }
+            // 4 S^T k-steps and 2 x 2 P V steps, each followed by one quarter of
+            // the softmax's exponentials
+#pragma unroll
+            for (int k = 0; k < DS + 2 * DT; ++k) {
+                __builtin_amdgcn_sched_barrier(0);
+                if (k < DS) {
+#pragma unroll
+                    for (int qt = 0; qt < QT; ++qt)
+                        s_nxt[qt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kop[k], qop[qt][k], s_nxt[qt], 0, 0, 0);
+                } else {
+                    const int dt = (k - DS) >> 1, ks = (k - DS) & 1;
+#pragma unroll
+                    for (int qt = 0; qt < QT; ++qt)
+                        oacc[qt][dt] =
+                            __builtin_amdgcn_mfma_f32_32x32x16_bf16(vop[dt][ks], p_prev[qt][ks], oacc[qt][dt], 0, 0, 0);
+                }
+                // softmax quarter(s): 4 x QT groups of 4 scores spread over the steps
+                constexpr int NQ = 4 * QT;
+                constexpr int NSTEP = DS + 2 * DT;
+#pragma unroll
+                for (int q = 0; q < NQ; ++q) {
+                    if (q * NSTEP / NQ == k) {
+                        const int qt = q / 4, part = q % 4;
+                        lsum[qt] += probs4(s_cur[qt], 4 * part, m_run[qt] * c2, pp[qt][part >> 1], 4 * (part & 1));
+                    }
+                }
+            }
+            __builtin_amdgcn_sched_barrier(0);
+        }
+        softmax_tail(s_cur, pp, lsum, mx);
+#pragma unroll
+        for (int qt = 0; qt < QT; ++qt) {
+            p_prev[qt][0] = pp[qt][0];
+            p_prev[qt][1] = pp[qt][1];
+            s_cur[qt] = s_nxt[qt];
+        }
+        if (t + 1 < n_chunk) mask(b_t1, s_cur);
+        b_t = b_t1;
+        b_t1 = cn2;
+    }
+    if (RESHAPE && !r_issued) {  // a block with no kept key block
+        issue_rows(a.resid, 0);
+        r_issued = 1;
     }
     wait_vm<0>();
-    if (!RESHAPE) r_st = st;  // any stage serves as the output tile
+    if (n_chunk > 0) pv((n_chunk - 1) & 1, p_prev);  // P V of the last chunk
 
     // ---- epilogue: O = factor * acc (+ R) into the tile in LDS, then row stores -----
-    lds_u8* const Ot = lds + r_st * STAGE;
+    lds_u8* const Ot = lds;  // residual / output tile over the K stages
 #pragma unroll
     for (int qt = 0; qt < QT; ++qt) {
         const int rl = qt * 32 + l32;  // row within the block
