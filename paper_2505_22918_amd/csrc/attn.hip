@@ -15,33 +15,38 @@
 // Computing the transposed products keeps every query in one lane column: the
 // 32x32 accumulator of S^T hands each lane 16 keys of one query, which are
 // exactly the 8+8 key values the B operand of the P V product needs, so P
-// never leaves registers.  The row max needs one exchange between lane l and
-// l^32 (v_permlane32_swap).
+// never leaves registers.  The rows of the V^T operand are permuted so that
+// each lane's 16 accumulator values of O^T are 16 consecutive head dims of
+// its query: the residual tile arrives and the output leaves as 16-byte
+// vector loads and stores straight from registers.
 //
-// Memory.  K and V chunks move from HBM/L2 straight into a two-stage LDS ring
-// with buffer_load ... lds (no staging registers); chunk i+1 is in flight while
-// chunk i is computed.  A buffer resource per chunk ends at the last key row,
-// so rows past T arrive as zeros (their scores are then masked to -inf).  Rows
-// stay row-major in LDS: K is read as the A operand with 16-byte reads, V^T
-// through ds_read_b64_tr_b16, the CDNA4 LDS transpose read.  16-byte slots of a
-// row are XOR-swizzled by row so both reads are free of bank conflicts (72-wide
-// heads use 144-byte rows, which spread banks as is).  The first chunk's DMA is
-// in flight together with the Q and rho loads; once the last chunk has been
-// issued, the residual tile R of the query block is brought into the stage that
-// falls free, so the epilogue finds it in LDS.
+// Memory.  Q arrives by buffer loads straight into its B-operand registers.
+// K and V chunks move from HBM/L2 into a two-stage LDS ring with
+// buffer_load ... lds (no staging registers); chunks t+1 and t+2 of K and t of
+// V are in flight while chunk t is computed.  Buffer resources end at the last
+// key row, so rows past T arrive as zeros (their scores are then masked).
+// Rows stay row-major in LDS: K is read as the A operand with 16-byte reads,
+// V^T through ds_read_b64_tr_b16, the CDNA4 LDS transpose read.  16-byte slots
+// of a row are XOR-swizzled by row so both reads are free of bank conflicts
+// (72-wide heads use 144-byte rows, which spread banks as is).
 //
-// Softmax.  The running max m_run starts at the first chunk's max and moves
-// only when a chunk's probabilities against it reach 2^64 (far below fp32 and
-// bf16 overflow); that rare case rescales O and l and recomputes the chunk.
-// Without requested statistics no per-chunk max is taken at all: the overflow
-// test reads the chunk's row sum.  With statistics the exact max is tracked and
-// l is moved to it at the end, so the emitted pair is exactly max and exp-sum.
+// Software pipeline.  Step t issues the DMA of K(t+2) and V(t), then runs
+// S(t+1) = K Q^T and the P V product of chunk t-1 on the matrix cores, spread
+// over the vector work of chunk t's softmax.  The last step has no S product;
+// the residual loads are issued there.
 //
-// Epilogue.  O = factor * acc (+ R) is formed in registers against R read from
-// LDS, written back as bf16 over R in place, and leaves as 16-byte row stores.
+// Softmax.  The running max starts at the first chunk's max and moves only
+// when a chunk's probabilities against it reach 2^64 (far below fp32 and bf16
+// overflow); that rare case rescales O and l and recomputes the chunk.
+// Without requested statistics no per-chunk max is taken:
+// the overflow test reads the chunk's row sum.  With statistics the exact max
+// is tracked and l is moved to it at the end, so the emitted pair is exactly
+// max and exp-sum.
 
 #include <hip/hip_runtime.h>
 #include <stdint.h>
+
+#include <type_traits>
 
 #include "kernels.h"
 
@@ -50,18 +55,17 @@ namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef int i32x4 __attribute__((ext_vector_type(4)));
 typedef const __attribute__((address_space(4))) int32_t* csr_ptr;
 typedef __attribute__((address_space(3))) unsigned char lds_u8;
 typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
 typedef __attribute__((address_space(3))) bf16x8 lds_bf16x8;
-typedef __attribute__((address_space(3))) u32x2 lds_u32x2;
-typedef __attribute__((address_space(3))) u32x4 lds_u32x4;
 
 constexpr float kJump = 18446744073709551616.0f;  // 2^64: stale-max limit on a probability
+constexpr int kOob = 0x40000000;                   // buffer offset past every record: reads zero
 
 // Geometry of one 32-key chunk of K or V in LDS.
 template <int D>
@@ -81,16 +85,17 @@ struct Geo<72> {
     static constexpr bool SWZ = false;
 };
 
-// K rows (and the R / O tile): 8 consecutive rows read the same slot -> XOR with r & 7.
+// K rows: 8 consecutive rows read the same slot -> XOR with r & 7.
 template <int D>
 __device__ __forceinline__ int kswz(int r) {
     return Geo<D>::SWZ ? (r & 7) : 0;
 }
-// V rows: a transpose read covers 4 consecutive rows x 2 adjacent slots -> XOR
-// with 2 * (r & 3) keeps those 8 (row, slot) pairs on distinct banks.
+// V rows: a transpose read covers 4 consecutive rows and, per row, the two
+// slots s and s ^ 2 -> XOR with {0, 1, 4, 5}[r & 3] keeps the 8 (row, slot)
+// pairs of a half-wave on distinct banks.
 template <int D>
 __device__ __forceinline__ int vswz(int r) {
-    return Geo<D>::SWZ ? ((r & 3) << 1) : 0;
+    return Geo<D>::SWZ ? (((r & 2) << 1) | (r & 1)) : 0;
 }
 
 __device__ __forceinline__ float pair_max(float x) {
@@ -106,8 +111,8 @@ __device__ __forceinline__ float pair_sum(float x) {
 __device__ __forceinline__ float lo_f(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float hi_f(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
 __device__ __forceinline__ uint32_t pack_bf16(float a, float b) {
-    const bf16x4 v = {(__bf16)a, (__bf16)b, (__bf16)0.f, (__bf16)0.f};
-    return __builtin_bit_cast(u32x2, v)[0];
+    const bf16x2 v = {(__bf16)a, (__bf16)b};
+    return __builtin_bit_cast(uint32_t, v);
 }
 
 // s_waitcnt with only the vector-memory counter constrained (gfx9 encoding:
@@ -133,6 +138,16 @@ __device__ __forceinline__ void dma16(uint32_t lds_addr, int voff, i32x4 rsrc) {
         : "memory");
 }
 
+// 16 bytes per lane from buffer `rsrc` at byte offset `voff` into registers.
+// The data lands later: the caller waits on the vector-memory counter and
+// then passes the value through settle() before reading it.
+__device__ __forceinline__ u32x4 vload16(int voff, i32x4 rsrc) {
+    u32x4 v;
+    asm volatile("buffer_load_dwordx4 %0, %1, %2, 0 offen" : "=&v"(v) : "v"(voff), "s"(rsrc) : "memory");
+    return v;
+}
+__device__ __forceinline__ void settle(u32x4& v) { asm volatile("" : "+v"(v)); }
+
 __device__ __forceinline__ i32x4 buffer_rsrc(const void* base, int bytes) {
     const uint64_t p = (uint64_t)(uintptr_t)base;
     return i32x4{(int)(uint32_t)p, (int)((uint32_t)(p >> 32) & 0xffffu), bytes, 0x00020000};
@@ -151,15 +166,12 @@ void attn_fwd(AttnArgs a) {
     constexpr int DS = DK / 16;              // k-steps of Q K^T
     constexpr int DT = DV / 32;              // 32-row tiles of O^T
     constexpr int DC = D / 8;                // 16-byte chunks per token row
-    constexpr int ROWB = G::SLOTS * 16;      // LDS bytes per K / V / R row (= 2 * D)
+    constexpr int ROWB = G::SLOTS * 16;      // LDS bytes per K / V row (= 2 * D)
     constexpr int TILE = 32 * ROWB;          // LDS bytes per K or V chunk
-    constexpr int STAGE = 2 * TILE;          // one ring stage: K then V
     constexpr int NSLOT = 32 * G::SLOTS;     // 16-byte slots per chunk and tensor
     constexpr int NDMA = (NSLOT + 63) / 64;  // DMA instructions per chunk and tensor
-    constexpr int RSLOT = BS * DC;           // 16-byte slots of the R tile
-    constexpr int NDMA_R = (RSLOT + 63) / 64;
-    constexpr int SMEM = 2 * STAGE + 256;    // two stages + slack for padded V^T reads
-    static_assert(RSLOT * 16 <= 2 * TILE, "Q / R tile fits two stages");
+    constexpr int NR = QT * DT * 2;          // residual loads per lane
+    constexpr int SMEM = 4 * TILE + 256;     // K and V stages + slack for padded V^T reads
     static_assert(ROWB == 2 * D, "rows are unpadded");
 
     __shared__ __attribute__((aligned(1024))) unsigned char smem[SMEM];
@@ -182,6 +194,7 @@ void attn_fwd(AttnArgs a) {
     const uint16_t* __restrict__ Kh = a.k + head_off;
     const uint16_t* __restrict__ Vh = a.v + head_off;
     const int row0 = qb * BS;  // first query row of the block
+    const int nrow = (T - row0) < BS ? (T - row0) : BS;
 
     // ---- per-lane constant offsets ------------------------------------------------
     // DMA: lane fills 16-byte LDS slot n*64 + lane of a chunk, i.e. (row r, slot s),
@@ -203,19 +216,25 @@ void attn_fwd(AttnArgs a) {
         ch = ch < DC ? ch : DC - 1;
         k_rd[s] = l32 * ROWB + ((ch ^ kswz<D>(l32)) * 16);
     }
-    // V^T A-operand transpose reads: in each group of 16 lanes, lane L supplies row
-    // 4*hi + L/4 (+16ks, +8 for the second read) at head-dim 32dt + 16(group & 1) +
-    // 4(L & 3); every lane then receives 4 consecutive rows at head-dim 32dt + l32.
+    // V^T A-operand transpose reads.  In a group of 16 lanes (G4 = lane / 16),
+    // lane L supplies key row 4*hi + L/4 (+16ks, +8 for the second read) at the
+    // 4 head dims starting at 32dt + 16(L & 1) + 8(G4 & 1) + 4((L >> 1) & 1).
+    // Lane 4a + b of the group then receives 4 consecutive keys of head dim
+    // 32dt + 16(a & 1) + 8(G4 & 1) + 4(a >> 1) + b, which puts head dim
+    // 32dt + 16h + 4j + i on O^T accumulator row 8j + 4h + i: lane (h, col)
+    // accumulates head dims 32dt + 16h .. +15 of query col.
     int v_rd[DT];
     {
         const int G4 = lane >> 4, L = lane & 15;
         const int r = 4 * hi + (L >> 2);
 #pragma unroll
         for (int dt = 0; dt < DT; ++dt) {
-            const int d = 32 * dt + 16 * (G4 & 1) + 4 * (L & 3);
+            const int d = 32 * dt + 16 * (L & 1) + 8 * (G4 & 1) + 4 * ((L >> 1) & 1);
             v_rd[dt] = r * ROWB + (((d >> 3) ^ vswz<D>(r)) * 16) + (d & 7) * 2;
         }
     }
+    // rows of this block in Q / R / O; rows past T read as zeros
+    const i32x4 q_rs = buffer_rsrc(a.q + head_off + (size_t)row0 * D, nrow * D * 2);
 
     // ---- kept key blocks of this query block ----------------------------------------
     int e_beg, e_end;
@@ -253,16 +272,15 @@ void attn_fwd(AttnArgs a) {
     };
 
     // LDS map: K stages at [0, TILE) and [TILE, 2 TILE), V stages at [2 TILE, 3 TILE)
-    // and [3 TILE, 4 TILE).  Before the walk the Q tile sits in the V stages; after
-    // the last K chunk has been read the residual / output tile takes the K stages.
+    // and [3 TILE, 4 TILE); chunk t uses stage t & 1 of each.
     auto k_off = [&](int st) { return st * TILE; };
     auto v_off = [&](int st) { return (2 + st) * TILE; };
 
     // DMA of the 32-key chunk of `head` starting at key `base` to LDS byte offset
     // `dst`; the buffer ends at row T, so rows past it read as zeros.  A chunk that
-    // holds no key (base < 0) is not loaded.
-    auto issue = [&](const uint16_t* head, const int (&off)[NDMA], int base, int dst) {
-        if (base < 0) return;
+    // holds no key (base < 0) is not loaded.  Returns the number of loads issued.
+    auto issue = [&](const uint16_t* head, const int (&off)[NDMA], int base, int dst) -> int {
+        if (base < 0) return 0;
         const int left = (T - base) * (D * 2);
         const int nrec = left < 32 * D * 2 ? left : 32 * D * 2;
         const i32x4 rs = buffer_rsrc(head + (size_t)base * D, nrec);
@@ -270,37 +288,34 @@ void attn_fwd(AttnArgs a) {
         for (int n = 0; n < NDMA; ++n) {
             if (NSLOT % 64 == 0 || n * 64 + lane < NSLOT) dma16(lds0 + dst + n * 1024, off[n], rs);
         }
+        return NDMA;
     };
-    // DMA of the block's BS rows of `tensor` (Q or R) to LDS byte offset `dst`, same
-    // row layout and swizzle as K (rows past T read as zeros)
-    auto issue_rows = [&](const uint16_t* tensor, int dst) {
-        const int left = (T - row0) * (D * 2);
-        const int nrec = left < BS * D * 2 ? left : BS * D * 2;
-        const i32x4 rr = buffer_rsrc(tensor + head_off + (size_t)row0 * D, nrec);
-#pragma unroll
-        for (int n = 0; n < NDMA_R; ++n) {
-            const int slot = n * 64 + lane;
-            const int r = slot / DC, s = slot - (slot / DC) * DC;
-            if (RSLOT % 64 == 0 || slot < RSLOT)
-                dma16(lds0 + dst + n * 1024, r * (D * 2) + ((s ^ kswz<D>(r)) * 16), rr);
-        }
-    };
-
-    // wait until at most n vector-memory operations (the ones just issued) are
-    // outstanding; waiting for fewer is always safe, so take the largest constant <= n
+    // wait until at most n (0, NDMA or 2 NDMA) vector-memory loads are outstanding
     auto wait_le = [&](int n) {
-        if (n >= 2 * NDMA + NDMA_R) {
-            wait_vm<2 * NDMA + NDMA_R>();
-        } else if (n >= NDMA + NDMA_R) {
-            wait_vm<NDMA + NDMA_R>();
-        } else if (n >= 2 * NDMA) {
+        if (n >= 2 * NDMA) {
             wait_vm<2 * NDMA>();
-        } else if (n >= NDMA_R) {
-            wait_vm<NDMA_R>();
         } else if (n >= NDMA) {
             wait_vm<NDMA>();
         } else {
             wait_vm<0>();
+        }
+    };
+    // residual tile in the O^T accumulator layout: lane (hi, l32) of tile (qt, dt)
+    // takes row 32qt + l32, head dims 32dt + 16hi .. +15 as two 16-byte loads
+    u32x4 rraw[QT][DT][2];
+    auto issue_resid = [&]() {
+        const i32x4 rs = buffer_rsrc(a.resid + head_off + (size_t)row0 * D, nrow * D * 2);
+#pragma unroll
+        for (int qt = 0; qt < QT; ++qt) {
+#pragma unroll
+            for (int dt = 0; dt < DT; ++dt) {
+#pragma unroll
+                for (int u = 0; u < 2; ++u) {
+                    const int ch = 4 * dt + 2 * hi + u;
+                    const int off = ch < DC ? (qt * 32 + l32) * (D * 2) + ch * 16 : kOob;
+                    rraw[qt][dt][u] = vload16(off, rs);
+                }
+            }
         }
     };
 
@@ -311,31 +326,31 @@ void attn_fwd(AttnArgs a) {
         const int row = row0 + qt * 32 + l32;
         rho_r[qt] = (RESHAPE && row < T) ? a.rho[(size_t)bh * T + row] : 0.f;
     }
-    const int c0 = n_chunk > 0 ? chunk_base(0) : -1;
-    int c1 = n_chunk > 1 ? chunk_base(1) : -1;
-    issue(Kh, kdma, c0, k_off(0));
-    issue_rows(a.q, v_off(0));
-    issue(Kh, kdma, c1, k_off(1));
-    if (c1 >= 0) {
-        wait_vm<NDMA>();  // K(0) and the Q tile have landed; K(1) may be in flight
-    } else {
-        wait_vm<0>();
-    }
-
-    // Q^T operands from the Q tile: lane holds query l32 of tile qt, head dims
-    // 16s + 8hi .. +7 (zero past D)
-    bf16x8 qop[QT][DS];
+    // Q^T operands: lane holds query l32 of tile qt, head dims 16s + 8hi .. +7
+    // (zero past D and past T)
+    u32x4 qraw[QT][DS];
 #pragma unroll
     for (int qt = 0; qt < QT; ++qt) {
-        const int rl = qt * 32 + l32;
 #pragma unroll
         for (int s = 0; s < DS; ++s) {
             const int ch = 2 * s + hi;
-            if (ch < DC) {
-                qop[qt][s] = *(const lds_bf16x8*)(lds + v_off(0) + rl * ROWB + ((ch ^ kswz<D>(rl)) * 16));
-            } else {
-                qop[qt][s] = bf16x8{};
-            }
+            qraw[qt][s] = vload16(ch < DC ? (qt * 32 + l32) * (D * 2) + ch * 16 : kOob, q_rs);
+        }
+    }
+    const int c0 = n_chunk > 0 ? chunk_base(0) : -1;
+    const int c1 = n_chunk > 1 ? chunk_base(1) : -1;
+    issue(Kh, kdma, c0, k_off(0));
+    int after = issue(Vh, vdma, c0, v_off(0));
+    after += issue(Kh, kdma, c1, k_off(1));
+    if (RESHAPE && n_chunk == 0) issue_resid();
+    wait_le(after);  // Q and K(0) have landed
+    bf16x8 qop[QT][DS];
+#pragma unroll
+    for (int qt = 0; qt < QT; ++qt) {
+#pragma unroll
+        for (int s = 0; s < DS; ++s) {
+            settle(qraw[qt][s]);
+            qop[qt][s] = __builtin_bit_cast(bf16x8, qraw[qt][s]);
         }
     }
 
@@ -378,35 +393,49 @@ void attn_fwd(AttnArgs a) {
             }
         }
     };
-    // O^T += V^T P^T for the V chunk in stage `st`; the V^T operand is two
-    // transpose reads of 4 rows each
-    auto pv = [&](int st, const bf16x8 (&pp)[QT][2]) {
+    // V^T operand of k-step ks of the V chunk in stage `st`: two transpose reads
+    // of 4 key rows each
+    auto v_operand = [&](int st, int dt, int ks) -> bf16x8 {
         const lds_u8* Vs = lds + v_off(st);
+        const bf16x4 v0 = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(Vs + v_rd[dt] + 16 * ks * ROWB));
+        const bf16x4 v1 = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(Vs + v_rd[dt] + (16 * ks + 8) * ROWB));
+        return __builtin_shufflevector(v0, v1, 0, 1, 2, 3, 4, 5, 6, 7);
+    };
+    // O^T += V^T P^T for the V chunk in stage `st`
+    auto pv = [&](int st, const bf16x8 (&pp)[QT][2]) {
 #pragma unroll
         for (int dt = 0; dt < DT; ++dt) {
 #pragma unroll
             for (int ks = 0; ks < 2; ++ks) {
-                const bf16x4 v0 = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(Vs + v_rd[dt] + 16 * ks * ROWB));
-                const bf16x4 v1 =
-                    __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(Vs + v_rd[dt] + (16 * ks + 8) * ROWB));
-                const bf16x8 vv = __builtin_shufflevector(v0, v1, 0, 1, 2, 3, 4, 5, 6, 7);
+                const bf16x8 vv = v_operand(st, dt, ks);
 #pragma unroll
                 for (int qt = 0; qt < QT; ++qt)
                     oacc[qt][dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vv, pp[qt][ks], oacc[qt][dt], 0, 0, 0);
             }
         }
     };
-    // probabilities of 4 scores against the running max: bf16 operand values and
-    // their fp32 sum
-    auto probs4 = [&](const f32x16& sc, int x0, float mc, bf16x8& pp, int y0) {
-        float acc = 0.f;
+    // probabilities of scores x0 .. x0+3 against the running max (mc = m * c2),
+    // as bf16 operand values; their fp32 sum starts (first) or joins acc
+    auto probs4 = [&](const f32x16& sc, int x0, float mc, float& acc, bool first) -> bf16x4 {
+        float p[4];
 #pragma unroll
-        for (int x = 0; x < 4; ++x) {
-            const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[x0 + x], c2, -mc));
-            acc += p;
-            pp[y0 + x] = (__bf16)p;
-        }
-        return acc;
+        for (int x = 0; x < 4; ++x) p[x] = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[x0 + x], c2, -mc));
+        const float part = (p[0] + p[1]) + (p[2] + p[3]);
+        acc = first ? part : acc + part;
+        const bf16x2 lo = {(__bf16)p[0], (__bf16)p[1]};
+        const bf16x2 hi2 = {(__bf16)p[2], (__bf16)p[3]};
+        return __builtin_shufflevector(lo, hi2, 0, 1, 2, 3);
+    };
+    // the whole chunk's probabilities of tile qt
+    auto probs16 = [&](const f32x16& sc, float mc, bf16x8 (&pq)[2]) -> float {
+        float s0, s1;
+        const bf16x4 g0 = probs4(sc, 0, mc, s0, true);
+        const bf16x4 g1 = probs4(sc, 4, mc, s1, true);
+        const bf16x4 g2 = probs4(sc, 8, mc, s0, false);
+        const bf16x4 g3 = probs4(sc, 12, mc, s1, false);
+        pq[0] = __builtin_shufflevector(g0, g1, 0, 1, 2, 3, 4, 5, 6, 7);
+        pq[1] = __builtin_shufflevector(g2, g3, 0, 1, 2, 3, 4, 5, 6, 7);
+        return s0 + s1;
     };
     // row max of one chunk; lane holds keys 8j + 4hi + i for acc index 4j + i, the
     // other 16 keys of its query sit in lane l ^ 32
@@ -417,9 +446,9 @@ void attn_fwd(AttnArgs a) {
         mx = fmaxf(mx, sc[15]);
         return pair_max(mx);
     };
-    // softmax of chunk scores `sc` against the running max; the rare case of a
-    // probability reaching 2^64 rescales O and l and recomputes (all PV products
-    // issued so far are in oacc by then)
+    // close the softmax of chunk scores `sc`: the rare case of a probability
+    // reaching 2^64 rescales O and l and recomputes (all P V products issued so
+    // far are in oacc by then); then l takes the chunk's sum
     auto softmax_tail = [&](f32x16 (&sc)[QT], bf16x8 (&pp)[QT][2], float (&lsum)[QT], float (&mx)[QT]) {
         bool jump = false;
 #pragma unroll
@@ -434,114 +463,64 @@ void attn_fwd(AttnArgs a) {
 #pragma unroll
                 for (int dt = 0; dt < DT; ++dt) oacc[qt][dt] *= alpha;
                 m_run[qt] = mnew;
-                const float mc = mnew * c2;
-                lsum[qt] = probs4(sc[qt], 0, mc, pp[qt][0], 0) + probs4(sc[qt], 4, mc, pp[qt][0], 4) +
-                           probs4(sc[qt], 8, mc, pp[qt][1], 0) + probs4(sc[qt], 12, mc, pp[qt][1], 4);
+                lsum[qt] = probs16(sc[qt], mnew * c2, pp[qt]);
             }
         }
 #pragma unroll
         for (int qt = 0; qt < QT; ++qt) l_run[qt] += lsum[qt];
     };
 
-    // Software pipeline over chunks 0 .. n-1.  Step t issues the DMA of K(t+2) and
-    // V(t) (into the stages K(t) and V(t-2) have left), then runs S(t+1) = K Q^T and
-    // the P V product of chunk t-1 on the matrix cores, spread over the vector work
-    // of chunk t's softmax.  The residual / output tile replaces the K stages once
-    // the last K chunk has been read.
+    // ---- software pipeline over chunks 0 .. n-1 -----------------------------------
     f32x16 s_cur[QT];
     bf16x8 p_prev[QT][2];
-    int r_issued = 0;
     if (n_chunk > 0) {
         qk(0, s_cur);
         mask(c0, s_cur);
-    }
-    // step 0: as the later steps, without a P V product yet
-    {
-        const int c2n = n_chunk > 2 ? chunk_base(2) : -1;
-        issue(Kh, kdma, c2n, k_off(0));  // K(0) has been read
-        issue(Vh, vdma, c0, v_off(0));   // the Q tile has been read
-        int now = (c2n >= 0 ? NDMA : 0) + (c0 >= 0 ? NDMA : 0);
-        if (RESHAPE && n_chunk <= 1) {  // no K chunk left to read
-            issue_rows(a.resid, 0);
-            r_issued = 1;
-            now += NDMA_R;
-        }
-        wait_le(now);  // K(1)
-        if (n_chunk > 0) {
-            f32x16 s_nxt[QT];
-            float lsum[QT], mx[QT];
-            bf16x8 pp[QT][2];
-            if (n_chunk > 1) qk(1, s_nxt);
 #pragma unroll
-            for (int qt = 0; qt < QT; ++qt) {
-                if (STATS) {
-                    mx[qt] = chunk_max(s_cur[qt]);
-                    m_top[qt] = fmaxf(m_top[qt], mx[qt]);
-                }
-                const float mc = m_run[qt] * c2;
-                lsum[qt] = probs4(s_cur[qt], 0, mc, pp[qt][0], 0) + probs4(s_cur[qt], 4, mc, pp[qt][0], 4) +
-                           probs4(s_cur[qt], 8, mc, pp[qt][1], 0) + probs4(s_cur[qt], 12, mc, pp[qt][1], 4);
-            }
-            softmax_tail(s_cur, pp, lsum, mx);
-#pragma unroll
-            for (int qt = 0; qt < QT; ++qt) {
-                p_prev[qt][0] = pp[qt][0];
-                p_prev[qt][1] = pp[qt][1];
-            }
-            if (n_chunk > 1) {
-#pragma unroll
-                for (int qt = 0; qt < QT; ++qt) s_cur[qt] = s_nxt[qt];
-                mask(c1, s_cur);
-            }
-        }
+        for (int qt = 0; qt < QT; ++qt) m_run[qt] = fmaxf(chunk_max(s_cur[qt]), -1e30f);
     }
     // rolling window of chunk bases: b_t = base(t), b_t1 = base(t+1)
-    int b_t = n_chunk > 1 ? c1 : -1;
-    int b_t1 = n_chunk > 2 ? chunk_base(2) : -1;
-    for (int t = 1; t < n_chunk; ++t) {
-        const int kst = t & 1;  // stage of K(t) and V(t)
-        // refill: K(t+2) -> stage of K(t), V(t) -> stage of V(t-2); the residual
-        // tile takes the K stages once the last K chunk (t) was read in step t-1
-        const int cn2 = t + 2 < n_chunk ? chunk_base(t + 2) : -1;
-        const int ct = b_t;
-        issue(Kh, kdma, cn2, k_off(kst));
-        issue(Vh, vdma, ct, v_off(kst));
-        if (RESHAPE && t == n_chunk - 1) {
-            issue_rows(a.resid, 0);
-            r_issued = 1;
-        }
-        // K(t+1) and V(t-1) were issued one step earlier
-        wait_le((cn2 >= 0 ? NDMA : 0) + (ct >= 0 ? NDMA : 0) + ((RESHAPE && t == n_chunk - 1) ? NDMA_R : 0));
+    int b_t = c0, b_t1 = c1;
 
-        // interleaved block: S(t+1) and P V(t-1) on the matrix cores, softmax(t) on
-        // the vector unit (after the last chunk the S product reads a stale stage
-        // and is discarded)
+    // Step t: issue K(t+2) (HAS_QK) and V(t) (t > 0; V(0) left with the
+    // prologue), wait for K(t+1) and V(t-1), then S(t+1) (HAS_QK) and P V(t-1)
+    // (HAS_PV) on the matrix cores, interleaved with softmax(t).  The step
+    // without S product is the last one; it issues the residual loads.
+    auto step = [&](int t, auto has_qk, auto has_pv) {
+        constexpr bool HAS_QK = decltype(has_qk)::value;
+        constexpr bool HAS_PV = decltype(has_pv)::value;
+        const int kst = t & 1;  // stage of K(t) and V(t)
+        int cn2 = -1;
+        int after = 0;
+        if (HAS_QK) {
+            cn2 = t + 2 < n_chunk ? chunk_base(t + 2) : -1;
+            after += issue(Kh, kdma, cn2, k_off(kst));  // K(t) was read in step t-1
+        }
+        if (t > 0) after += issue(Vh, vdma, b_t, v_off(kst));  // V(t-2) was read in step t-1
+        wait_le(after);
+        if (!HAS_QK && RESHAPE) issue_resid();
+
         f32x16 s_nxt[QT];
         float lsum[QT], mx[QT];
         bf16x8 pp[QT][2];
         {
-            const lds_u8* Ks = lds + k_off(kst ^ 1);
-            const lds_u8* Vs = lds + v_off(kst ^ 1);
             bf16x8 kop[DS];
+            if (HAS_QK) {
+                const lds_u8* Ks = lds + k_off(kst ^ 1);
 #pragma unroll
-            for (int s = 0; s < DS; ++s) kop[s] = *(const lds_bf16x8*)(Ks + k_rd[s]);
+                for (int s = 0; s < DS; ++s) kop[s] = *(const lds_bf16x8*)(Ks + k_rd[s]);
+            }
             bf16x8 vop[DT][2];
+            if (HAS_PV) {
 #pragma unroll
-            for (int dt = 0; dt < DT; ++dt) {
+                for (int dt = 0; dt < DT; ++dt) {
 #pragma unroll
-                for (int ks = 0; ks < 2; ++ks) {
-                    const bf16x4 v0 =
-                        __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(Vs + v_rd[dt] + 16 * ks * ROWB));
-                    const bf16x4 v1 =
-                        __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(Vs + v_rd[dt] + (16 * ks + 8) * ROWB));
-                    vop[dt][ks] = __builtin_shufflevector(v0, v1, 0, 1, 2, 3, 4, 5, 6, 7);
+                    for (int ks = 0; ks < 2; ++ks) vop[dt][ks] = v_operand(kst ^ 1, dt, ks);
                 }
             }
+            float sa[QT], sb[QT];
 #pragma unroll
-            for (int qt = 0; qt < QT; ++qt) {
-                s_nxt[qt] = f32x16{};
-                lsum[qt] = 0.f;
-            }
+            for (int qt = 0; qt < QT; ++qt) s_nxt[qt] = f32x16{};
             if (STATS) {
 #pragma unroll
                 for (int qt = 0; qt < QT; ++qt) {
@@ -549,55 +528,89 @@ void attn_fwd(AttnArgs a) {
                     m_top[qt] = fmaxf(m_top[qt], mx[qt]);
                 }
             }
-            // 4 S^T k-steps and 2 x 2 P V steps, each followed by one quarter of
-            // the softmax's exponentials
+            // MFMA pairs (S^T k-steps, then P V steps), each followed by its share
+            // of the 4 x QT groups of 4 exponentials
+            constexpr int NSTEP = (HAS_QK ? DS : 0) + (HAS_PV ? 2 * DT : 0);
+            constexpr int NSLOTS = NSTEP > 0 ? NSTEP : 1;
+            constexpr int NQ = 4 * QT;
+            bf16x4 grp[QT][4];
 #pragma unroll
-            for (int k = 0; k < DS + 2 * DT; ++k) {
+            for (int k = 0; k < NSLOTS; ++k) {
                 __builtin_amdgcn_sched_barrier(0);
-                if (k < DS) {
+                if (k < NSTEP) {
+                    if (HAS_QK && k < DS) {
 #pragma unroll
-                    for (int qt = 0; qt < QT; ++qt)
-                        s_nxt[qt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kop[k], qop[qt][k], s_nxt[qt], 0, 0, 0);
-                } else {
-                    const int dt = (k - DS) >> 1, ks = (k - DS) & 1;
+                        for (int qt = 0; qt < QT; ++qt)
+                            s_nxt[qt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kop[k], qop[qt][k], s_nxt[qt], 0, 0, 0);
+                    } else {
+                        const int kk = k - (HAS_QK ? DS : 0);
+                        const int dt = kk >> 1, ks = kk & 1;
 #pragma unroll
-                    for (int qt = 0; qt < QT; ++qt)
-                        oacc[qt][dt] =
-                            __builtin_amdgcn_mfma_f32_32x32x16_bf16(vop[dt][ks], p_prev[qt][ks], oacc[qt][dt], 0, 0, 0);
+                        for (int qt = 0; qt < QT; ++qt)
+                            oacc[qt][dt] =
+                                __builtin_amdgcn_mfma_f32_32x32x16_bf16(vop[dt][ks], p_prev[qt][ks], oacc[qt][dt], 0, 0, 0);
+                    }
                 }
-                // softmax quarter(s): 4 x QT groups of 4 scores spread over the steps
-                constexpr int NQ = 4 * QT;
-                constexpr int NSTEP = DS + 2 * DT;
 #pragma unroll
                 for (int q = 0; q < NQ; ++q) {
-                    if (q * NSTEP / NQ == k) {
+                    if (q * NSLOTS / NQ == k) {
                         const int qt = q / 4, part = q % 4;
-                        lsum[qt] += probs4(s_cur[qt], 4 * part, m_run[qt] * c2, pp[qt][part >> 1], 4 * (part & 1));
+                        grp[qt][part] =
+                            probs4(s_cur[qt], 4 * part, m_run[qt] * c2, (part & 1) ? sb[qt] : sa[qt], part < 2);
                     }
                 }
             }
             __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+            for (int qt = 0; qt < QT; ++qt) {
+                lsum[qt] = sa[qt] + sb[qt];
+                pp[qt][0] = __builtin_shufflevector(grp[qt][0], grp[qt][1], 0, 1, 2, 3, 4, 5, 6, 7);
+                pp[qt][1] = __builtin_shufflevector(grp[qt][2], grp[qt][3], 0, 1, 2, 3, 4, 5, 6, 7);
+            }
         }
         softmax_tail(s_cur, pp, lsum, mx);
 #pragma unroll
         for (int qt = 0; qt < QT; ++qt) {
             p_prev[qt][0] = pp[qt][0];
             p_prev[qt][1] = pp[qt][1];
-            s_cur[qt] = s_nxt[qt];
+            if (HAS_QK) s_cur[qt] = s_nxt[qt];
         }
-        if (t + 1 < n_chunk) mask(b_t1, s_cur);
+        if (HAS_QK) mask(b_t1, s_cur);
         b_t = b_t1;
         b_t1 = cn2;
+    };
+
+    using yes = std::true_type;
+    using no = std::false_type;
+    if (n_chunk == 1) {
+        step(0, no{}, no{});
+    } else if (n_chunk > 1) {
+        step(0, yes{}, no{});
+        for (int t = 1; t < n_chunk - 1; ++t) step(t, yes{}, yes{});
+        step(n_chunk - 1, no{}, yes{});
     }
-    if (RESHAPE && !r_issued) {  // a block with no kept key block
-        issue_rows(a.resid, 0);
-        r_issued = 1;
+    if (n_chunk > 0) {
+        // V(n-1) has landed once only the residual loads may be outstanding
+        if (RESHAPE) {
+            wait_vm<NR>();
+        } else {
+            wait_vm<0>();
+        }
+        pv((n_chunk - 1) & 1, p_prev);  // P V of the last chunk
     }
     wait_vm<0>();
-    if (n_chunk > 0) pv((n_chunk - 1) & 1, p_prev);  // P V of the last chunk
+    if (RESHAPE) {
+#pragma unroll
+        for (int qt = 0; qt < QT; ++qt) {
+#pragma unroll
+            for (int dt = 0; dt < DT; ++dt) {
+                settle(rraw[qt][dt][0]);
+                settle(rraw[qt][dt][1]);
+            }
+        }
+    }
 
-    // ---- epilogue: O = factor * acc (+ R) into the tile in LDS, then row stores -----
-    lds_u8* const Ot = lds;  // residual / output tile over the K stages
+    // ---- epilogue: O = factor * acc (+ R), 16-byte row stores from registers --------
 #pragma unroll
     for (int qt = 0; qt < QT; ++qt) {
         const int rl = qt * 32 + l32;  // row within the block
@@ -613,32 +626,26 @@ void attn_fwd(AttnArgs a) {
 #pragma unroll
         for (int dt = 0; dt < DT; ++dt) {
 #pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                const int d = 32 * dt + 8 * j + 4 * hi;
-                if (d < D) {
-                    lds_u32x2* p = (lds_u32x2*)(Ot + rl * ROWB + (((d >> 3) ^ kswz<D>(rl)) * 16) + (d & 7) * 2);
-                    float y[4];
+            for (int u = 0; u < 2; ++u) {
+                const int ch = 4 * dt + 2 * hi + u;  // head dims 8ch .. 8ch+7
+                if (ch < DC && row < T) {
+                    float y[8];
 #pragma unroll
-                    for (int i = 0; i < 4; ++i) y[i] = oacc[qt][dt][4 * j + i] * factor;
+                    for (int e = 0; e < 8; ++e) y[e] = oacc[qt][dt][8 * u + e] * factor;
                     if (RESHAPE) {
-                        const u32x2 r2 = *p;
-                        y[0] += lo_f(r2[0]);
-                        y[1] += hi_f(r2[0]);
-                        y[2] += lo_f(r2[1]);
-                        y[3] += hi_f(r2[1]);
+                        const u32x4 r4 = rraw[qt][dt][u];
+#pragma unroll
+                        for (int w = 0; w < 4; ++w) {
+                            y[2 * w] += lo_f(r4[w]);
+                            y[2 * w + 1] += hi_f(r4[w]);
+                        }
                     }
-                    *p = u32x2{pack_bf16(y[0], y[1]), pack_bf16(y[2], y[3])};
+                    const u32x4 o4 = {pack_bf16(y[0], y[1]), pack_bf16(y[2], y[3]), pack_bf16(y[4], y[5]),
+                                      pack_bf16(y[6], y[7])};
+                    *reinterpret_cast<u32x4*>(a.o + head_off + (size_t)row * D + 8 * ch) = o4;
                 }
             }
         }
-    }
-    // rows leave as 16-byte stores
-    for (int u = lane; u < BS * DC; u += 64) {
-        const int rl = u / DC, ch = u - (u / DC) * DC;
-        const int row = row0 + rl;
-        if (row >= T) continue;
-        const u32x4 v = *(const lds_u32x4*)(Ot + rl * ROWB + ((ch ^ kswz<D>(rl)) * 16));
-        *reinterpret_cast<u32x4*>(a.o + head_off + (size_t)row * D + 8 * ch) = v;
     }
 }
 
