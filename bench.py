@@ -16,6 +16,7 @@ Prints ONE JSON line on stdout; progress goes to stderr.
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
 import math
 import os
@@ -36,23 +37,6 @@ def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
-def host_csr(wl):
-    """Row counts of the workload's mask: the same closed forms the library uses
-    (counts only; the CSR itself is built on the GPU)."""
-    from paper_2505_22918_amd import synth
-
-    nb = wl.n_blk
-    if wl.kind == synth.PAT_LOCAL2D:
-        return np.full(nb, min(wl.keep, nb))
-    if wl.kind == synth.PAT_VIDEO3D:
-        ntb = -(-wl.n_text // wl.block)
-        cnt = np.full(nb, ntb + min(wl.keep, nb - ntb))
-        cnt[:ntb] = ntb
-        return cnt
-    m = synth.explicit_block_mask(nb, wl.seed)
-    return m.sum(axis=1)
-
-
 def kept_flops(wl, row_ptr, col_idx):
     """4 * rows(qb) * cols(kb) * D summed over kept block pairs, times B*H."""
     sizes = np.minimum(wl.block, wl.T - np.arange(wl.n_blk) * wl.block)
@@ -61,6 +45,41 @@ def kept_flops(wl, row_ptr, col_idx):
         cols = col_idx[row_ptr[qb]:row_ptr[qb + 1]]
         tot += int(sizes[qb]) * int(sizes[cols].sum())
     return 4.0 * tot * wl.D * wl.B * wl.H
+
+
+def executed_flops(wl, n_kept):
+    """MFMA FLOPs the kernel issues: whole 32-key chunks and whole query blocks, at
+    the padded contraction (80 for a 72-wide head) and padded O^T rows (96)."""
+    dk, dv = (64, 64) if wl.D == 64 else (80, 96)
+    chunks = n_kept * (wl.block // 32)
+    return float(chunks) * 2.0 * wl.block * 32 * (dk + dv) * wl.B * wl.H
+
+
+def kernel_source_sha256():
+    """Digest of the attention kernel's sources; a counter summary applies only to
+    the kernel it was taken from."""
+    h = hashlib.sha256()
+    for name in ("attn.hip", "kernels.h"):
+        with open(os.path.join(ROOT, "paper_2505_22918_amd", "csrc", name), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def measured_traffic(wl_name):
+    """HBM bytes per launch of the fused kernel from the committed rocprofv3 counter
+    summary (FETCH_SIZE + WRITE_SIZE, calibrated against a plain copy), or None when
+    there is none for this workload or the kernel has changed since."""
+    path = os.path.join(ROOT, "profiles", f"attn_fwd_{wl_name}_hbm_traffic.md")
+    if not os.path.exists(path):
+        return None
+    sha = kernel_source_sha256()
+    with open(path) as f:
+        for line in f:
+            if line.startswith("bench-traffic:"):
+                kv = dict(t.split("=", 1) for t in line.split()[1:])
+                if kv.get("workload") == wl_name and kv.get("kernel_sha256") == sha:
+                    return int(kv["fetch_bytes"]) + int(kv["write_bytes"])
+    return None
 
 
 def fused_bytes(wl, stats=False):
@@ -127,6 +146,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-path", action="store_true", help="skip timing the other calls of the path")
     ap.add_argument("--cpu-budget", type=float, default=12.0)
+    ap.add_argument("--cold-iters", type=int, default=5,
+                    help="calls timed one by one after a 512 MiB write that flushes L2 and MALL")
     ap.add_argument("--copy-mb", type=int, default=0,
                     help="also run K plain device copies of this many MiB (HBM counter calibration)")
     args = ap.parse_args()
@@ -198,6 +219,29 @@ def main():
     log(f"fused sparse+reshape: {ms_call * 1e3:.1f} us/call, {tflops:.1f} TFLOP/s "
         f"({tflops / PEAK_BF16_TFLOPS:.1%} of bf16 peak), {gbs:.0f} GB/s algorithmic")
 
+    # outside the timed region: per-call medians, warm (inputs in L2/MALL from
+    # the previous call) and cold (a 512 MiB write evicts L2 and MALL first)
+    def one_call_ms(pre=None):
+        if pre is not None:
+            pre()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        fused()
+        b.record(stream)
+        torch.cuda.synchronize()
+        return a.elapsed_time(b)
+
+    warm_ms = [one_call_ms() for _ in range(max(1, min(args.steps, 50)))]
+    cold_ms = []
+    if args.cold_iters > 0:
+        flush = torch.empty(256 << 20, dtype=torch.bfloat16, device=dev)
+        cold_ms = [one_call_ms(lambda i=i: flush.fill_(float(i % 7))) for i in range(args.cold_iters)]
+        del flush
+    warm_med = float(np.median(warm_ms))
+    cold_med = float(np.median(cold_ms)) if cold_ms else None
+    log(f"per-call median: warm {warm_med * 1e3:.1f} us"
+        + (f", cold {cold_med * 1e3:.1f} us" if cold_med is not None else ""))
+
     if args.copy_mb > 0:
         n = args.copy_mb * (1 << 20) // 2
         src = torch.empty(n, dtype=torch.bfloat16, device=dev).fill_(1.0)
@@ -255,17 +299,22 @@ def main():
         log(f"cpu oracle: {cpu}")
 
     bound = "hbm" if ai < ridge else "mfma"
+    traffic = measured_traffic(wl.name)
+    exec_flops = executed_flops(wl, mask.nnz)
     roof = {
         "bound": bound,
         "achieved": gbs if bound == "hbm" else tflops,
         "peak": PEAK_HBM_GBS if bound == "hbm" else PEAK_BF16_TFLOPS,
         "unit": "GB/s" if bound == "hbm" else "TFLOP/s",
         "frac": (gbs / PEAK_HBM_GBS) if bound == "hbm" else (tflops / PEAK_BF16_TFLOPS),
-        "traffic": None,
-        "kernel": "attn_fwd<D,block,reshape=true>",
+        "traffic": traffic,
+        "traffic_over_algorithmic": (traffic / nbytes) if traffic else None,
+        "kernel": f"attn_fwd<{wl.D},{wl.block},reshape=true,stats=false>",
         "algorithmic_bytes": nbytes,
         "algorithmic_flops": flops,
+        "executed_mfma_flops": exec_flops,
         "arith_intensity": ai,
+        "ridge": ridge,
     }
     rec = {
         "metric": "sparse+reshape attention ms/call and kept-block TFLOP/s (% bf16 MFMA peak)",
@@ -276,6 +325,8 @@ def main():
         "warmup": args.warmup,
         "ms_per_step": ms_call,
         "ms_per_call": ms_call,
+        "warm_median_ms": warm_med,
+        "cold_median_ms": cold_med,
         "host_ms_per_step": t_wall,
         "mfma_frac": tflops / PEAK_BF16_TFLOPS,
         "higher_is_better": True,
