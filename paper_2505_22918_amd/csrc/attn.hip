@@ -21,19 +21,22 @@
 // vector loads and stores straight from registers.
 //
 // Memory.  Q arrives by buffer loads straight into its B-operand registers.
-// K and V chunks move from HBM/L2 into a two-stage LDS ring with
-// buffer_load ... lds (no staging registers); chunks t+1 and t+2 of K and t of
-// V are in flight while chunk t is computed.  Buffer resources end at the last
-// key row, so rows past T arrive as zeros (their scores are then masked).
+// K and V chunks move from HBM/L2 into LDS rings (three K stages, two V stages,
+// 20 KB per wave at D = 64) with buffer_load ... lds (no staging registers);
+// K(t+2), K(t+3) and V(t) are in flight while chunk t is softmaxed.  Buffer
+// resources end at the last key row, so rows past T arrive as zeros (their
+// scores are then masked).
 // Rows stay row-major in LDS: K is read as the A operand with 16-byte reads,
 // V^T through ds_read_b64_tr_b16, the CDNA4 LDS transpose read.  16-byte slots
 // of a row are XOR-swizzled by row so both reads are free of bank conflicts
 // (72-wide heads use 144-byte rows, which spread banks as is).
 //
-// Software pipeline.  Step t issues the DMA of K(t+2) and V(t), then runs
-// S(t+1) = K Q^T and the P V product of chunk t-1 on the matrix cores, spread
-// over the vector work of chunk t's softmax.  The last step has no S product;
-// the residual loads are issued there.
+// Software pipeline.  Step t issues the DMA of V(t) and K(t+3), then runs the
+// P V product of chunk t-1 on the matrix cores under the exponentials of chunk
+// t's softmax, packs chunk t's probabilities to bf16 in the registers P V(t-1)
+// has just read, and computes S(t+1) = K Q^T into the registers softmax(t) has
+// just read (no register copies between steps).  The last step has no S
+// product; the residual loads are issued there.
 //
 // Softmax.  The running max starts at the first chunk's max and moves only
 // when a chunk's probabilities against it reach 2^64 (far below fp32 and bf16
@@ -138,6 +141,21 @@ __device__ __forceinline__ void dma16(uint32_t lds_addr, int voff, i32x4 rsrc) {
         : "memory");
 }
 
+// Four such loads at byte offsets voff + 1024 n into LDS m0 + 1024 n + 16 * lane,
+// n = 0..3: the instruction offset moves both the source and the LDS destination.
+__device__ __forceinline__ void dma16x4(uint32_t lds_addr, int voff, i32x4 rsrc) {
+    asm volatile(
+        "s_mov_b32 m0, %0\n\t"
+        "s_nop 0\n\t"
+        "buffer_load_dwordx4 %1, %2, 0 offen lds\n\t"
+        "buffer_load_dwordx4 %1, %2, 0 offen offset:1024 lds\n\t"
+        "buffer_load_dwordx4 %1, %2, 0 offen offset:2048 lds\n\t"
+        "buffer_load_dwordx4 %1, %2, 0 offen offset:3072 lds"
+        :
+        : "s"(lds_addr), "v"(voff), "s"(rsrc)
+        : "memory");
+}
+
 // 16 bytes per lane from buffer `rsrc` at byte offset `voff` into registers.
 // The data lands later: the caller waits on the vector-memory counter and
 // then passes the value through settle() before reading it.
@@ -171,7 +189,9 @@ void attn_fwd(AttnArgs a) {
     constexpr int NSLOT = 32 * G::SLOTS;     // 16-byte slots per chunk and tensor
     constexpr int NDMA = (NSLOT + 63) / 64;  // DMA instructions per chunk and tensor
     constexpr int NR = QT * DT * 2;          // residual loads per lane
-    constexpr int SMEM = 4 * TILE + 256;     // K and V stages + slack for padded V^T reads
+    // three K stages and two V stages (+ slack for the padded V^T reads of a 72-wide
+    // head): 20 KB per wave at D = 64, so 8 waves fill a CU's 160 KB
+    constexpr int SMEM = 5 * TILE + (D == 64 ? 0 : 256);
     static_assert(ROWB == 2 * D, "rows are unpadded");
 
     __shared__ __attribute__((aligned(1024))) unsigned char smem[SMEM];
@@ -271,33 +291,31 @@ void attn_fwd(AttnArgs a) {
         return (kb >= 0 && kb < a.n_blk && base < T) ? base : -1;
     };
 
-    // LDS map: K stages at [0, TILE) and [TILE, 2 TILE), V stages at [2 TILE, 3 TILE)
-    // and [3 TILE, 4 TILE); chunk t uses stage t & 1 of each.
+    // LDS map: K(t) in stage t % 3 at [0, 3 TILE), V(t) in stage t % 2 at
+    // [3 TILE, 5 TILE).
     auto k_off = [&](int st) { return st * TILE; };
-    auto v_off = [&](int st) { return (2 + st) * TILE; };
+    auto v_off = [&](int st) { return (3 + st) * TILE; };
 
     // DMA of the 32-key chunk of `head` starting at key `base` to LDS byte offset
     // `dst`; the buffer ends at row T, so rows past it read as zeros.  A chunk that
-    // holds no key (base < 0) is not loaded.  Returns the number of loads issued.
-    auto issue = [&](const uint16_t* head, const int (&off)[NDMA], int base, int dst) -> int {
-        if (base < 0) return 0;
-        const int left = (T - base) * (D * 2);
-        const int nrec = left < 32 * D * 2 ? left : 32 * D * 2;
-        const i32x4 rs = buffer_rsrc(head + (size_t)base * D, nrec);
-#pragma unroll
-        for (int n = 0; n < NDMA; ++n) {
-            if (NSLOT % 64 == 0 || n * 64 + lane < NSLOT) dma16(lds0 + dst + n * 1024, off[n], rs);
+    // holds no key (base < 0) gets an empty buffer: its loads read zeros and touch
+    // no memory.  Every call issues NDMA loads, so all waits below are constants.
+    auto issue = [&](const uint16_t* head, const int (&off)[NDMA], int base, int dst) {
+        const uint16_t* src = head;
+        int nrec = 0;
+        if (base >= 0) {
+            const int left = (T - base) * (D * 2);
+            nrec = left < 32 * D * 2 ? left : 32 * D * 2;
+            src = head + (size_t)base * D;
         }
-        return NDMA;
-    };
-    // wait until at most n (0, NDMA or 2 NDMA) vector-memory loads are outstanding
-    auto wait_le = [&](int n) {
-        if (n >= 2 * NDMA) {
-            wait_vm<2 * NDMA>();
-        } else if (n >= NDMA) {
-            wait_vm<NDMA>();
+        const i32x4 rs = buffer_rsrc(src, nrec);
+        if (NSLOT == 4 * 64) {
+            dma16x4(lds0 + dst, off[0], rs);
         } else {
-            wait_vm<0>();
+#pragma unroll
+            for (int n = 0; n < NDMA; ++n) {
+                if (NSLOT % 64 == 0 || n * 64 + lane < NSLOT) dma16(lds0 + dst + n * 1024, off[n], rs);
+            }
         }
     };
     // residual tile in the O^T accumulator layout: lane (hi, l32) of tile (qt, dt)
@@ -339,11 +357,16 @@ void attn_fwd(AttnArgs a) {
     }
     const int c0 = n_chunk > 0 ? chunk_base(0) : -1;
     const int c1 = n_chunk > 1 ? chunk_base(1) : -1;
+    const int c2b = n_chunk > 2 ? chunk_base(2) : -1;
+    // issue order Q, K(0), V(0), K(1), K(2); afterwards each step issues V(t) then
+    // K(t+3), so waiting for V(t-1) in step t leaves exactly three chunk loads
+    // (K(t+2), V(t), K(t+3)) in flight
     issue(Kh, kdma, c0, k_off(0));
-    int after = issue(Vh, vdma, c0, v_off(0));
-    after += issue(Kh, kdma, c1, k_off(1));
+    issue(Vh, vdma, c0, v_off(0));
+    issue(Kh, kdma, c1, k_off(1));
+    issue(Kh, kdma, c2b, k_off(2));
+    wait_vm<3 * NDMA>();  // Q and K(0) have landed
     if (RESHAPE && n_chunk == 0) issue_resid();
-    wait_le(after);  // Q and K(0) have landed
     bf16x8 qop[QT][DS];
 #pragma unroll
     for (int qt = 0; qt < QT; ++qt) {
@@ -414,28 +437,35 @@ void attn_fwd(AttnArgs a) {
             }
         }
     };
-    // probabilities of scores x0 .. x0+3 against the running max (mc = m * c2),
-    // as bf16 operand values; their fp32 sum starts (first) or joins acc
-    auto probs4 = [&](const f32x16& sc, int x0, float mc, float& acc, bool first) -> bf16x4 {
-        float p[4];
+    // fp32 probabilities of scores x0 .. x0+3 against the running max (mc = m * c2);
+    // their sum starts (first) or joins acc
+    auto exps4 = [&](const f32x16& sc, int x0, float mc, float* p, float& acc, bool first) {
 #pragma unroll
         for (int x = 0; x < 4; ++x) p[x] = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[x0 + x], c2, -mc));
         const float part = (p[0] + p[1]) + (p[2] + p[3]);
         acc = first ? part : acc + part;
-        const bf16x2 lo = {(__bf16)p[0], (__bf16)p[1]};
-        const bf16x2 hi2 = {(__bf16)p[2], (__bf16)p[3]};
-        return __builtin_shufflevector(lo, hi2, 0, 1, 2, 3);
     };
-    // the whole chunk's probabilities of tile qt
-    auto probs16 = [&](const f32x16& sc, float mc, bf16x8 (&pq)[2]) -> float {
+    // all 16 probabilities of tile qt; returns their sum
+    auto exps16 = [&](const f32x16& sc, float mc, float (&p)[16]) -> float {
         float s0, s1;
-        const bf16x4 g0 = probs4(sc, 0, mc, s0, true);
-        const bf16x4 g1 = probs4(sc, 4, mc, s1, true);
-        const bf16x4 g2 = probs4(sc, 8, mc, s0, false);
-        const bf16x4 g3 = probs4(sc, 12, mc, s1, false);
-        pq[0] = __builtin_shufflevector(g0, g1, 0, 1, 2, 3, 4, 5, 6, 7);
-        pq[1] = __builtin_shufflevector(g2, g3, 0, 1, 2, 3, 4, 5, 6, 7);
+        exps4(sc, 0, mc, p + 0, s0, true);
+        exps4(sc, 4, mc, p + 4, s1, true);
+        exps4(sc, 8, mc, p + 8, s0, false);
+        exps4(sc, 12, mc, p + 12, s1, false);
         return s0 + s1;
+    };
+    // bf16 B operands of the P V product: keys 0-7 and 8-15 of the lane's 16
+    auto pack16 = [&](const float (&p)[16], bf16x8 (&pk)[2]) {
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            const bf16x2 a0 = {(__bf16)p[8 * h + 0], (__bf16)p[8 * h + 1]};
+            const bf16x2 a1 = {(__bf16)p[8 * h + 2], (__bf16)p[8 * h + 3]};
+            const bf16x2 a2 = {(__bf16)p[8 * h + 4], (__bf16)p[8 * h + 5]};
+            const bf16x2 a3 = {(__bf16)p[8 * h + 6], (__bf16)p[8 * h + 7]};
+            const bf16x4 lo = __builtin_shufflevector(a0, a1, 0, 1, 2, 3);
+            const bf16x4 hi4 = __builtin_shufflevector(a2, a3, 0, 1, 2, 3);
+            pk[h] = __builtin_shufflevector(lo, hi4, 0, 1, 2, 3, 4, 5, 6, 7);
+        }
     };
     // row max of one chunk; lane holds keys 8j + 4hi + i for acc index 4j + i, the
     // other 16 keys of its query sit in lane l ^ 32
@@ -446,138 +476,138 @@ void attn_fwd(AttnArgs a) {
         mx = fmaxf(mx, sc[15]);
         return pair_max(mx);
     };
-    // close the softmax of chunk scores `sc`: the rare case of a probability
-    // reaching 2^64 rescales O and l and recomputes (all P V products issued so
-    // far are in oacc by then); then l takes the chunk's sum
-    auto softmax_tail = [&](f32x16 (&sc)[QT], bf16x8 (&pp)[QT][2], float (&lsum)[QT], float (&mx)[QT]) {
+
+    // ---- software pipeline over chunks 0 .. n-1 -----------------------------------
+    // s holds the scores of the chunk being softmaxed, pk the bf16 probabilities of
+    // the chunk before it; both are updated in place each step.
+    f32x16 s[QT];
+    bf16x8 pk[QT][2];
+    if (n_chunk > 0) {
+        qk(0, s);
+        mask(c0, s);
+#pragma unroll
+        for (int qt = 0; qt < QT; ++qt) m_run[qt] = fmaxf(chunk_max(s[qt]), -1e30f);
+    }
+    // rolling window of chunk bases b_t = base(t), b_t1, b_t2; k3 = t % 3
+    int b_t = c0, b_t1 = c1, b_t2 = c2b;
+    int k3 = 0;
+
+    // Step t: issue V(t) (t > 0; V(0) left with the prologue) and K(t+3) (HAS_QK),
+    // and wait for K(t+1) and V(t-1).  Then
+    //   A: P V(t-1) (HAS_PV) on the matrix cores, interleaved with the
+    //      exponentials and row sums of softmax(t) in fp32;
+    //   the rare rescale (a probability reached 2^64: O and l move to the new
+    //      max, chunk t is recomputed; P V(t-1) is in O by then);
+    //   B: chunk t's bf16 probabilities into pk (P V(t-1) has read it), then
+    //      S(t+1) = K Q^T (HAS_QK) into s (softmax(t) has read it).
+    // The step without S product is the last one; it issues the residual loads.
+    auto step = [&](int t, auto has_qk, auto has_pv) {
+        constexpr bool HAS_QK = decltype(has_qk)::value;
+        constexpr bool HAS_PV = decltype(has_pv)::value;
+        const int vst = t & 1;                // stage of V(t)
+        const int kn = k3 == 2 ? 0 : k3 + 1;  // stage of K(t+1)
+        int cn3 = -1;
+        if (t > 0) issue(Vh, vdma, b_t, v_off(vst));  // V(t-2) was read in step t-1
+        if (HAS_QK) {
+            cn3 = t + 3 < n_chunk ? chunk_base(t + 3) : -1;
+            issue(Kh, kdma, cn3, k_off(k3));  // K(t) was read in step t-1
+        }
+        if (HAS_QK && HAS_PV) {
+            wait_vm<3 * NDMA>();  // K(t+2), V(t), K(t+3) may still fly
+        } else if (HAS_QK || HAS_PV) {
+            wait_vm<2 * NDMA>();  // step 0: K(2), K(3); last step: K(t+2), V(t)
+        }
+        if (!HAS_QK && RESHAPE) issue_resid();
+
+        bf16x8 vop[DT][2];
+        if (HAS_PV) {
+#pragma unroll
+            for (int dt = 0; dt < DT; ++dt) {
+#pragma unroll
+                for (int ks = 0; ks < 2; ++ks) vop[dt][ks] = v_operand(vst ^ 1, dt, ks);
+            }
+        }
+        bf16x8 kop[DS];
+        if (HAS_QK) {
+            const lds_u8* Ks = lds + k_off(kn);
+#pragma unroll
+            for (int ss = 0; ss < DS; ++ss) kop[ss] = *(const lds_bf16x8*)(Ks + k_rd[ss]);
+        }
+        float mx[QT];
+        if (STATS) {
+#pragma unroll
+            for (int qt = 0; qt < QT; ++qt) {
+                mx[qt] = chunk_max(s[qt]);
+                m_top[qt] = fmaxf(m_top[qt], mx[qt]);
+            }
+        }
+        // A: P V pairs, each followed by its share of the 4 x QT groups of 4
+        // exponentials
+        float pf[QT][16];
+        float sa[QT], sb[QT];
+        {
+            constexpr int NA = HAS_PV ? 2 * DT : 0;
+            constexpr int SLOTS = NA > 0 ? NA : 1;
+            constexpr int NQ = 4 * QT;
+#pragma unroll
+            for (int k = 0; k < SLOTS; ++k) {
+                __builtin_amdgcn_sched_barrier(0);
+                if (k < NA) {
+                    const int dt = k >> 1, ks = k & 1;
+#pragma unroll
+                    for (int qt = 0; qt < QT; ++qt)
+                        oacc[qt][dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vop[dt][ks], pk[qt][ks], oacc[qt][dt], 0, 0, 0);
+                }
+#pragma unroll
+                for (int q = 0; q < NQ; ++q) {
+                    if (q * SLOTS / NQ == k) {
+                        const int qt = q / 4, part = q % 4;
+                        exps4(s[qt], 4 * part, m_run[qt] * c2, pf[qt] + 4 * part, (part & 1) ? sb[qt] : sa[qt], part < 2);
+                    }
+                }
+            }
+            __builtin_amdgcn_sched_barrier(0);
+        }
+        float lsum[QT];
         bool jump = false;
 #pragma unroll
-        for (int qt = 0; qt < QT; ++qt) jump |= !(lsum[qt] < kJump);
+        for (int qt = 0; qt < QT; ++qt) {
+            lsum[qt] = sa[qt] + sb[qt];
+            jump |= !(lsum[qt] < kJump);
+        }
         if (__builtin_amdgcn_ballot_w64(jump)) {
 #pragma unroll
             for (int qt = 0; qt < QT; ++qt) {
-                if (!STATS) mx[qt] = chunk_max(sc[qt]);
+                if (!STATS) mx[qt] = chunk_max(s[qt]);
                 const float mnew = fmaxf(m_run[qt], mx[qt]);
                 const float alpha = __builtin_amdgcn_exp2f((m_run[qt] - mnew) * c2);
                 l_run[qt] *= alpha;
 #pragma unroll
                 for (int dt = 0; dt < DT; ++dt) oacc[qt][dt] *= alpha;
                 m_run[qt] = mnew;
-                lsum[qt] = probs16(sc[qt], mnew * c2, pp[qt]);
+                lsum[qt] = exps16(s[qt], mnew * c2, pf[qt]);
             }
         }
-#pragma unroll
-        for (int qt = 0; qt < QT; ++qt) l_run[qt] += lsum[qt];
-    };
-
-    // ---- software pipeline over chunks 0 .. n-1 -----------------------------------
-    f32x16 s_cur[QT];
-    bf16x8 p_prev[QT][2];
-    if (n_chunk > 0) {
-        qk(0, s_cur);
-        mask(c0, s_cur);
-#pragma unroll
-        for (int qt = 0; qt < QT; ++qt) m_run[qt] = fmaxf(chunk_max(s_cur[qt]), -1e30f);
-    }
-    // rolling window of chunk bases: b_t = base(t), b_t1 = base(t+1)
-    int b_t = c0, b_t1 = c1;
-
-    // Step t: issue K(t+2) (HAS_QK) and V(t) (t > 0; V(0) left with the
-    // prologue), wait for K(t+1) and V(t-1), then S(t+1) (HAS_QK) and P V(t-1)
-    // (HAS_PV) on the matrix cores, interleaved with softmax(t).  The step
-    // without S product is the last one; it issues the residual loads.
-    auto step = [&](int t, auto has_qk, auto has_pv) {
-        constexpr bool HAS_QK = decltype(has_qk)::value;
-        constexpr bool HAS_PV = decltype(has_pv)::value;
-        const int kst = t & 1;  // stage of K(t) and V(t)
-        int cn2 = -1;
-        int after = 0;
-        if (HAS_QK) {
-            cn2 = t + 2 < n_chunk ? chunk_base(t + 2) : -1;
-            after += issue(Kh, kdma, cn2, k_off(kst));  // K(t) was read in step t-1
-        }
-        if (t > 0) after += issue(Vh, vdma, b_t, v_off(kst));  // V(t-2) was read in step t-1
-        wait_le(after);
-        if (!HAS_QK && RESHAPE) issue_resid();
-
-        f32x16 s_nxt[QT];
-        float lsum[QT], mx[QT];
-        bf16x8 pp[QT][2];
-        {
-            bf16x8 kop[DS];
-            if (HAS_QK) {
-                const lds_u8* Ks = lds + k_off(kst ^ 1);
-#pragma unroll
-                for (int s = 0; s < DS; ++s) kop[s] = *(const lds_bf16x8*)(Ks + k_rd[s]);
-            }
-            bf16x8 vop[DT][2];
-            if (HAS_PV) {
-#pragma unroll
-                for (int dt = 0; dt < DT; ++dt) {
-#pragma unroll
-                    for (int ks = 0; ks < 2; ++ks) vop[dt][ks] = v_operand(kst ^ 1, dt, ks);
-                }
-            }
-            float sa[QT], sb[QT];
-#pragma unroll
-            for (int qt = 0; qt < QT; ++qt) s_nxt[qt] = f32x16{};
-            if (STATS) {
-#pragma unroll
-                for (int qt = 0; qt < QT; ++qt) {
-                    mx[qt] = chunk_max(s_cur[qt]);
-                    m_top[qt] = fmaxf(m_top[qt], mx[qt]);
-                }
-            }
-            // MFMA pairs (S^T k-steps, then P V steps), each followed by its share
-            // of the 4 x QT groups of 4 exponentials
-            constexpr int NSTEP = (HAS_QK ? DS : 0) + (HAS_PV ? 2 * DT : 0);
-            constexpr int NSLOTS = NSTEP > 0 ? NSTEP : 1;
-            constexpr int NQ = 4 * QT;
-            bf16x4 grp[QT][4];
-#pragma unroll
-            for (int k = 0; k < NSLOTS; ++k) {
-                __builtin_amdgcn_sched_barrier(0);
-                if (k < NSTEP) {
-                    if (HAS_QK && k < DS) {
-#pragma unroll
-                        for (int qt = 0; qt < QT; ++qt)
-                            s_nxt[qt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kop[k], qop[qt][k], s_nxt[qt], 0, 0, 0);
-                    } else {
-                        const int kk = k - (HAS_QK ? DS : 0);
-                        const int dt = kk >> 1, ks = kk & 1;
-#pragma unroll
-                        for (int qt = 0; qt < QT; ++qt)
-                            oacc[qt][dt] =
-                                __builtin_amdgcn_mfma_f32_32x32x16_bf16(vop[dt][ks], p_prev[qt][ks], oacc[qt][dt], 0, 0, 0);
-                    }
-                }
-#pragma unroll
-                for (int q = 0; q < NQ; ++q) {
-                    if (q * NSLOTS / NQ == k) {
-                        const int qt = q / 4, part = q % 4;
-                        grp[qt][part] =
-                            probs4(s_cur[qt], 4 * part, m_run[qt] * c2, (part & 1) ? sb[qt] : sa[qt], part < 2);
-                    }
-                }
-            }
-            __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-            for (int qt = 0; qt < QT; ++qt) {
-                lsum[qt] = sa[qt] + sb[qt];
-                pp[qt][0] = __builtin_shufflevector(grp[qt][0], grp[qt][1], 0, 1, 2, 3, 4, 5, 6, 7);
-                pp[qt][1] = __builtin_shufflevector(grp[qt][2], grp[qt][3], 0, 1, 2, 3, 4, 5, 6, 7);
-            }
-        }
-        softmax_tail(s_cur, pp, lsum, mx);
+        // B
 #pragma unroll
         for (int qt = 0; qt < QT; ++qt) {
-            p_prev[qt][0] = pp[qt][0];
-            p_prev[qt][1] = pp[qt][1];
-            if (HAS_QK) s_cur[qt] = s_nxt[qt];
+            l_run[qt] += lsum[qt];
+            pack16(pf[qt], pk[qt]);
         }
-        if (HAS_QK) mask(b_t1, s_cur);
+        if (HAS_QK) {
+#pragma unroll
+            for (int ss = 0; ss < DS; ++ss) {
+#pragma unroll
+                for (int qt = 0; qt < QT; ++qt)
+                    s[qt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kop[ss], qop[qt][ss], ss == 0 ? f32x16{} : s[qt], 0, 0,
+                                                                    0);
+            }
+            mask(b_t1, s);
+        }
         b_t = b_t1;
-        b_t1 = cn2;
+        b_t1 = b_t2;
+        b_t2 = cn3;
+        k3 = kn;
     };
 
     using yes = std::true_type;
@@ -596,7 +626,7 @@ void attn_fwd(AttnArgs a) {
         } else {
             wait_vm<0>();
         }
-        pv((n_chunk - 1) & 1, p_prev);  // P V of the last chunk
+        pv((n_chunk - 1) & 1, pk);  // P V of the last chunk
     }
     wait_vm<0>();
     if (RESHAPE) {
