@@ -257,6 +257,8 @@ def main():
         os2, _, _ = rt.attn_sparse(q2, k2, v2, mask)
         t_apply = time_calls(lambda: rt.reshape_apply(os2, rho, resid, 0.0, out=out), 10, stream)
         t_cache = time_calls(lambda: rt.cache_build(of, mf, lf, os_, ms, ls), 10, stream)
+        t_onepass = time_calls(lambda: rt.attn_cache(q1, k1, v1, mask, stats=False, out=out), 3, stream)
+        t_full_stats = time_calls(lambda: rt.attn_full(q1, k1, v1, block=wl.block, stats=True), 3, stream)
         if hm is not None:
             t_index = time_calls(lambda: rt.build_index(wl.T, wl.block, wl.kind, device=dev, host_mask=hm), 3,
                                  stream)
@@ -275,6 +277,8 @@ def main():
             "reshape_apply_ms": round(t_apply, 4),
             "reshape_apply_gbs": round(ew_bytes / (t_apply * 1e-3) / 1e9, 1),
             "unfused_ms": round(t_sparse + t_apply, 4),
+            "caching_step_three_calls_ms": round(t_full_stats + t_sparse + t_cache, 4),
+            "caching_step_one_pass_ms": round(t_onepass, 4),
             "speedup_vs_dense": round(t_dense / ms_call, 2),
         }
         log(f"path: {path}")

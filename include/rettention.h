@@ -128,6 +128,22 @@ rt_status rt_attn_sparse(const void* q, const void* k, const void* v, rt_dims di
                          const rt_bsr* mask, void* o, float* row_max, float* row_sum,
                          void* stream);
 
+/* One-pass caching step (App. A.3): dense attention over every key block,
+ * with the keys split by the mask into the kept set S and the rest, so that
+ * one walk gives the step's full output and the statistics cache:
+ *   O_full = softmax over all keys (Eq.1)                  -> o
+ *   rho    = sum_{j in S} e^{s_j} / sum_j e^{s_j}  (Eq.8)  -> rho
+ *   R      = sum_{j not in S} A_j v_j = O_full - rho O_S   -> resid (Eq.10)
+ * The kept blocks are walked first (their normalised output passes through o,
+ * which is then overwritten), the others after, against one running max.
+ * q, k, v: device bf16 [B,H,T,D]; o, resid: device bf16 [B,H,T,D] (written,
+ * must not alias q, k, v or each other); rho: device fp32 [B,H,T] (written);
+ * row_max / row_sum: device fp32 [B,H,T], the full-attention statistics, or
+ * NULL.  Rows whose query block keeps every key block get rho = 1, R = 0; a
+ * query block with no kept block gets rho = 0, R = O_full. */
+rt_status rt_attn_cache(const void* q, const void* k, const void* v, rt_dims dims, const rt_bsr* mask,
+                        void* o, float* row_max, float* row_sum, float* rho, void* resid, void* stream);
+
 /* Statistics cache at a caching (full-attention) step, Eq.8 and Eq.10:
  *   rho = (l_sparse / l_full) * exp(m_sparse - m_full)      (Eq.8)
  *   R   = O_full - rho * O_sparse                           (Eq.10)

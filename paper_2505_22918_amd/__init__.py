@@ -27,6 +27,7 @@ __all__ = [
     "build_index",
     "attn_full",
     "attn_sparse",
+    "attn_cache",
     "cache_build",
     "attn_sparse_reshape",
     "reshape_apply",
@@ -178,6 +179,25 @@ def attn_sparse(q, k, v, mask: BlockMask, stats=True, out=None):
     _lib.check("rt_attn_sparse", lib.rt_attn_sparse(_ptr(q), _ptr(k), _ptr(v), dims, ctypes.byref(bsr),
                                                     _ptr(o), _ptr(m), _ptr(l), _stream(q)))
     return (o, m, l) if stats else o
+
+
+def attn_cache(q, k, v, mask: BlockMask, stats=True, out=None):
+    """One-pass caching step (App. A.3): full attention over every key block with
+    the keys split by the mask.  Returns (O_full, rho, R[, m_full, l_full])."""
+    torch = _torch()
+    lib = _lib.load()
+    dims = _check_qkv(q, k, v)
+    o = out if out is not None else torch.empty_like(q)
+    rho = torch.empty(q.shape[:3], dtype=torch.float32, device=q.device)
+    resid = torch.empty_like(q)
+    m = l = None
+    if stats:
+        m = torch.empty_like(rho)
+        l = torch.empty_like(rho)
+    bsr = mask.c_struct()
+    _lib.check("rt_attn_cache", lib.rt_attn_cache(_ptr(q), _ptr(k), _ptr(v), dims, ctypes.byref(bsr), _ptr(o),
+                                                  _ptr(m), _ptr(l), _ptr(rho), _ptr(resid), _stream(q)))
+    return (o, rho, resid, m, l) if stats else (o, rho, resid)
 
 
 def cache_build(o_full, m_full, l_full, o_sparse, m_sparse, l_sparse):

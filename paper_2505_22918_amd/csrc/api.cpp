@@ -45,6 +45,8 @@ rt_status check_dims(const rt_dims& d, bool* empty) {
     const int64_t rows = (int64_t)d.B * d.H * d.T;
     if (rows * d.D >= (int64_t)1 << 40) return fail(RT_EINVAL, "tensor too large");
     if ((int64_t)d.B * d.H >= (int64_t)1 << 24) return fail(RT_EINVAL, "B*H too large");
+    // buffer record counts and offsets within one head are 32-bit
+    if ((int64_t)d.T * d.D * 2 >= (int64_t)1 << 31) return fail(RT_EINVAL, "T=%d too long for one head", d.T);
     *empty = rows == 0;
     return RT_OK;
 }
@@ -249,7 +251,7 @@ rt_status rt_attn_full(const void* q, const void* k, const void* v, rt_dims dims
     RT_TRY(check_items(dims, block));
     rt::AttnArgs a = base_args(q, k, v, dims, block, o, row_max, row_sum);
     a.dense = 1;
-    return hip_status(rt::launch_attention(a, dims.D, block, false, static_cast<hipStream_t>(stream)),
+    return hip_status(rt::launch_attention(a, dims.D, block, rt::kAttn, static_cast<hipStream_t>(stream)),
                       "full attention launch");
 }
 
@@ -267,8 +269,32 @@ rt_status rt_attn_sparse(const void* q, const void* k, const void* v, rt_dims di
     a.row_ptr = mask->row_ptr;
     a.col_idx = mask->col_idx;
     a.nnz = mask->nnz;
-    return hip_status(rt::launch_attention(a, dims.D, mask->block, false, static_cast<hipStream_t>(stream)),
+    return hip_status(rt::launch_attention(a, dims.D, mask->block, rt::kAttn, static_cast<hipStream_t>(stream)),
                       "sparse attention launch");
+}
+
+rt_status rt_attn_cache(const void* q, const void* k, const void* v, rt_dims dims, const rt_bsr* mask, void* o,
+                        float* row_max, float* row_sum, float* rho, void* resid, void* stream) {
+    bool empty = false;
+    RT_TRY(check_dims(dims, &empty));
+    RT_TRY(check_bsr(mask, dims));
+    if (empty) return ok();
+    RT_TRY(check_qkv(q, k, v, o));
+    RT_TRY(check_stat(rho, "rho"));
+    RT_TRY(check_tensor(resid, "resid"));
+    if (row_max) RT_TRY(check_stat(row_max, "row_max"));
+    if (row_sum) RT_TRY(check_stat(row_sum, "row_sum"));
+    if (resid == o || resid == q || resid == k || resid == v || o == q || o == k || o == v)
+        return fail(RT_EINVAL, "o and resid must not alias q, k, v or each other");
+    RT_TRY(check_items(dims, mask->block));
+    rt::AttnArgs a = base_args(q, k, v, dims, mask->block, o, row_max, row_sum);
+    a.row_ptr = mask->row_ptr;
+    a.col_idx = mask->col_idx;
+    a.nnz = mask->nnz;
+    a.rho_out = rho;
+    a.resid_out = static_cast<uint16_t*>(resid);
+    return hip_status(rt::launch_attention(a, dims.D, mask->block, rt::kAttnCache, static_cast<hipStream_t>(stream)),
+                      "caching-step launch");
 }
 
 rt_status rt_cache_build(const void* o_full, const float* m_full, const float* l_full, const void* o_sparse,
@@ -314,7 +340,7 @@ rt_status rt_attn_sparse_reshape(const void* q, const void* k, const void* v, rt
     a.rho = rho;
     a.resid = static_cast<const uint16_t*>(resid);
     a.rho_delta = rho_delta;
-    return hip_status(rt::launch_attention(a, dims.D, mask->block, true, static_cast<hipStream_t>(stream)),
+    return hip_status(rt::launch_attention(a, dims.D, mask->block, rt::kAttnReshape, static_cast<hipStream_t>(stream)),
                       "sparse+reshape launch");
 }
 

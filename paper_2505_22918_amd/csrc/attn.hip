@@ -174,7 +174,7 @@ __device__ __forceinline__ i32x4 buffer_rsrc(const void* base, int bytes) {
 template <int D, int BS>
 constexpr int kWaves = (D == 72 && BS == 64) ? 1 : 2;
 
-template <int D, int BS, bool RESHAPE, bool STATS>
+template <int D, int BS, bool RESHAPE, bool STATS, bool CACHE>
 __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(kWaves<D, BS>)))
 void attn_fwd(AttnArgs a) {
     using G = Geo<D>;
@@ -276,16 +276,41 @@ void attn_fwd(AttnArgs a) {
     if (!a.dense && lane < e_end - e_beg) cols = ((csr_ptr)a.col_idx)[e_beg + lane];
     wait_vm<0>();
     asm volatile("" : "+v"(cols));  // the load has landed; later reads need no wait
-    const int n_chunk = (e_end - e_beg) * (BS / 32);
+    // The caching step walks every key block: the kept ones first (chunks
+    // 0 .. n_in-1, CSR order), then the others in ascending order.
+    const int n_in = (e_end - e_beg) * (BS / 32);
+    const int n_chunk = CACHE ? a.n_blk * (BS / 32) : n_in;
+    auto kept_at = [&](int j) -> int {  // entry e_beg + j of the CSR row
+        return j < 64 ? __builtin_amdgcn_readlane(cols, j) : ((csr_ptr)a.col_idx)[e_beg + j];
+    };
+    int gen_kb = -1, gen_e = 0;  // complement walk: last block emitted, next kept entry
+    // Key base of chunk i, or -1 for a chunk holding no key.  Called for
+    // i = 0, 1, 2, ... in order, once each (the complement walk relies on it).
     auto chunk_base = [&](int i) -> int {
-        const int j = i / (BS / 32), half = i - j * (BS / 32);
-        int kb;
-        if (a.dense) {
-            kb = j;
-        } else if (j < 64) {
-            kb = __builtin_amdgcn_readlane(cols, j);
+        int kb, half;
+        if (CACHE && i >= n_in) {
+            const int jc = (i - n_in) / (BS / 32);
+            half = (i - n_in) - jc * (BS / 32);
+            if (half == 0) {
+                int c = gen_kb + 1;
+                while (gen_e < e_end - e_beg) {  // skip the kept blocks (sorted ascending)
+                    const int kk = kept_at(gen_e);
+                    if (kk < c) {
+                        ++gen_e;
+                    } else if (kk == c) {
+                        ++c;
+                        ++gen_e;
+                    } else {
+                        break;
+                    }
+                }
+                gen_kb = c;
+            }
+            kb = gen_kb;
         } else {
-            kb = ((csr_ptr)a.col_idx)[e_beg + j];
+            const int j = i / (BS / 32);
+            half = i - j * (BS / 32);
+            kb = a.dense ? j : kept_at(j);
         }
         const int base = kb * BS + 32 * half;
         return (kb >= 0 && kb < a.n_blk && base < T) ? base : -1;
@@ -380,11 +405,13 @@ void attn_fwd(AttnArgs a) {
     const float c2 = a.scale_log2;  // log2(e) / sqrt(D)
     f32x16 oacc[QT][DT];
     float m_run[QT], m_top[QT], l_run[QT];
+    float l_in[QT];  // caching step: kept-block exp-sum against m_run, once the kept walk is done
 #pragma unroll
     for (int qt = 0; qt < QT; ++qt) {
         m_run[qt] = -1e30f;  // finite: a fully masked chunk then yields p = 0, not NaN
         m_top[qt] = -INFINITY;
         l_run[qt] = 0.f;
+        l_in[qt] = 0.f;
 #pragma unroll
         for (int dt = 0; dt < DT; ++dt) oacc[qt][dt] = f32x16{};
     }
@@ -475,6 +502,36 @@ void attn_fwd(AttnArgs a) {
         for (int x = 3; x < 15; x += 2) mx = fmaxf(fmaxf(mx, sc[x]), sc[x + 1]);
         mx = fmaxf(mx, sc[15]);
         return pair_max(mx);
+    };
+
+    // Caching step, end of the kept walk: O_s = acc / l goes to the output rows
+    // (read back by the epilogue), l becomes l_in, and the walk over the other
+    // blocks starts a fresh sum and accumulator against the same running max.
+    auto flush_kept = [&]() {
+#pragma unroll
+        for (int qt = 0; qt < QT; ++qt) {
+            const int row = row0 + qt * 32 + l32;
+            const float inv = 1.0f / pair_sum(l_run[qt]);
+#pragma unroll
+            for (int dt = 0; dt < DT; ++dt) {
+#pragma unroll
+                for (int u = 0; u < 2; ++u) {
+                    const int ch = 4 * dt + 2 * hi + u;
+                    if (ch < DC && row < T) {
+                        const f32x16& acc = oacc[qt][dt];
+                        const u32x4 o4 = {pack_bf16(acc[8 * u + 0] * inv, acc[8 * u + 1] * inv),
+                                          pack_bf16(acc[8 * u + 2] * inv, acc[8 * u + 3] * inv),
+                                          pack_bf16(acc[8 * u + 4] * inv, acc[8 * u + 5] * inv),
+                                          pack_bf16(acc[8 * u + 6] * inv, acc[8 * u + 7] * inv)};
+                        *reinterpret_cast<u32x4*>(a.o + head_off + (size_t)row * D + 8 * ch) = o4;
+                    }
+                }
+            }
+            l_in[qt] = l_run[qt];
+            l_run[qt] = 0.f;
+#pragma unroll
+            for (int dt = 0; dt < DT; ++dt) oacc[qt][dt] = f32x16{};
+        }
     };
 
     // ---- software pipeline over chunks 0 .. n-1 -----------------------------------
@@ -568,6 +625,7 @@ void attn_fwd(AttnArgs a) {
             }
             __builtin_amdgcn_sched_barrier(0);
         }
+        if (CACHE && t == n_in && t > 0) flush_kept();  // P V of chunk n_in - 1 is in O
         float lsum[QT];
         bool jump = false;
 #pragma unroll
@@ -582,6 +640,7 @@ void attn_fwd(AttnArgs a) {
                 const float mnew = fmaxf(m_run[qt], mx[qt]);
                 const float alpha = __builtin_amdgcn_exp2f((m_run[qt] - mnew) * c2);
                 l_run[qt] *= alpha;
+                if (CACHE) l_in[qt] *= alpha;
 #pragma unroll
                 for (int dt = 0; dt < DT; ++dt) oacc[qt][dt] *= alpha;
                 m_run[qt] = mnew;
@@ -640,6 +699,85 @@ void attn_fwd(AttnArgs a) {
         }
     }
 
+    if (CACHE) {
+        // ---- caching-step epilogue (App. A.3): with l_in, l_out and acc_out
+        // against one running max, l_f = l_in + l_out, rho = l_in / l_f (Eq.8),
+        // R = acc_out / l_f = O_f - rho O_s (Eq.10), O_f = rho O_s + R (Eq.1)
+        const bool split = n_in < n_chunk;  // the other blocks were walked after a flush
+        u32x4 osraw[QT][DT][2];
+        if (split && n_in > 0) {  // O_s rows stored by the flush (complete: vmcnt is 0 here)
+            const i32x4 rs = buffer_rsrc(a.o + head_off + (size_t)row0 * D, nrow * D * 2);
+#pragma unroll
+            for (int qt = 0; qt < QT; ++qt) {
+#pragma unroll
+                for (int dt = 0; dt < DT; ++dt) {
+#pragma unroll
+                    for (int u = 0; u < 2; ++u) {
+                        const int ch = 4 * dt + 2 * hi + u;
+                        osraw[qt][dt][u] = vload16(ch < DC ? (qt * 32 + l32) * (D * 2) + ch * 16 : kOob, rs);
+                    }
+                }
+            }
+            wait_vm<0>();
+#pragma unroll
+            for (int qt = 0; qt < QT; ++qt) {
+#pragma unroll
+                for (int dt = 0; dt < DT; ++dt) {
+                    settle(osraw[qt][dt][0]);
+                    settle(osraw[qt][dt][1]);
+                }
+            }
+        } else {
+#pragma unroll
+            for (int qt = 0; qt < QT; ++qt) {
+#pragma unroll
+                for (int dt = 0; dt < DT; ++dt) osraw[qt][dt][0] = osraw[qt][dt][1] = u32x4{};
+            }
+        }
+#pragma unroll
+        for (int qt = 0; qt < QT; ++qt) {
+            const int row = row0 + qt * 32 + l32;
+            const float li = pair_sum(split ? l_in[qt] : l_run[qt]);
+            const float lo = split ? pair_sum(l_run[qt]) : 0.f;
+            const float lf = li + lo;
+            const float inv = 1.0f / lf;
+            const float rho = split ? li / lf : 1.0f;  // exactly 1 when every block is kept
+            if (hi == 0 && row < T) {
+                const size_t si = (size_t)bh * T + row;
+                a.rho_out[si] = rho;
+                if (STATS) {
+                    if (a.row_max) a.row_max[si] = m_top[qt] * a.scale_nat;
+                    if (a.row_sum) a.row_sum[si] = lf * __builtin_amdgcn_exp2f((m_run[qt] - m_top[qt]) * c2);
+                }
+            }
+#pragma unroll
+            for (int dt = 0; dt < DT; ++dt) {
+#pragma unroll
+                for (int u = 0; u < 2; ++u) {
+                    const int ch = 4 * dt + 2 * hi + u;
+                    if (ch < DC && row < T) {
+                        const u32x4 os4 = osraw[qt][dt][u];
+                        float r[8], of[8];
+#pragma unroll
+                        for (int e = 0; e < 8; ++e) {
+                            const float acc = oacc[qt][dt][8 * u + e] * inv;
+                            const float osv = (e & 1) ? hi_f(os4[e >> 1]) : lo_f(os4[e >> 1]);
+                            r[e] = split ? acc : 0.f;
+                            of[e] = split ? __builtin_fmaf(rho, osv, acc) : acc;
+                        }
+                        const size_t off = head_off + (size_t)row * D + 8 * ch;
+                        *reinterpret_cast<u32x4*>(a.resid_out + off) =
+                            u32x4{pack_bf16(r[0], r[1]), pack_bf16(r[2], r[3]), pack_bf16(r[4], r[5]),
+                                  pack_bf16(r[6], r[7])};
+                        *reinterpret_cast<u32x4*>(a.o + off) = u32x4{pack_bf16(of[0], of[1]), pack_bf16(of[2], of[3]),
+                                                                     pack_bf16(of[4], of[5]), pack_bf16(of[6], of[7])};
+                    }
+                }
+            }
+        }
+        return;
+    }
+
     // ---- epilogue: O = factor * acc (+ R), 16-byte row stores from registers --------
 #pragma unroll
     for (int qt = 0; qt < QT; ++qt) {
@@ -679,25 +817,32 @@ void attn_fwd(AttnArgs a) {
     }
 }
 
-template <int D, int BS, bool RESHAPE, bool STATS>
+template <int D, int BS, bool RESHAPE, bool STATS, bool CACHE>
 hipError_t launch_one(const AttnArgs& a, hipStream_t stream) {
     dim3 grid(8 * a.per_xcd), block(64);
-    hipLaunchKernelGGL((attn_fwd<D, BS, RESHAPE, STATS>), grid, block, 0, stream, a);
+    hipLaunchKernelGGL((attn_fwd<D, BS, RESHAPE, STATS, CACHE>), grid, block, 0, stream, a);
     return hipGetLastError();
 }
 
 template <int D, int BS>
-hipError_t launch_db(const AttnArgs& a, bool reshape, hipStream_t stream) {
+hipError_t launch_db(const AttnArgs& a, AttnMode mode, hipStream_t stream) {
     const bool stats = a.row_max != nullptr || a.row_sum != nullptr;
-    if (reshape) return stats ? launch_one<D, BS, true, true>(a, stream) : launch_one<D, BS, true, false>(a, stream);
-    return stats ? launch_one<D, BS, false, true>(a, stream) : launch_one<D, BS, false, false>(a, stream);
+    switch (mode) {
+        case kAttnReshape:
+            return stats ? launch_one<D, BS, true, true, false>(a, stream) : launch_one<D, BS, true, false, false>(a, stream);
+        case kAttnCache:
+            return stats ? launch_one<D, BS, false, true, true>(a, stream) : launch_one<D, BS, false, false, true>(a, stream);
+        default:
+            return stats ? launch_one<D, BS, false, true, false>(a, stream)
+                         : launch_one<D, BS, false, false, false>(a, stream);
+    }
 }
 
 }  // namespace
 
-hipError_t launch_attention(const AttnArgs& a, int D, int block, bool reshape, hipStream_t stream) {
-    if (D == 64) return block == 64 ? launch_db<64, 64>(a, reshape, stream) : launch_db<64, 32>(a, reshape, stream);
-    return block == 64 ? launch_db<72, 64>(a, reshape, stream) : launch_db<72, 32>(a, reshape, stream);
+hipError_t launch_attention(const AttnArgs& a, int D, int block, AttnMode mode, hipStream_t stream) {
+    if (D == 64) return block == 64 ? launch_db<64, 64>(a, mode, stream) : launch_db<64, 32>(a, mode, stream);
+    return block == 64 ? launch_db<72, 64>(a, mode, stream) : launch_db<72, 32>(a, mode, stream);
 }
 
 }  // namespace rt

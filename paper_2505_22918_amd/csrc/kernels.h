@@ -27,9 +27,16 @@ struct AttnArgs {
     int32_t per_xcd;    // ceil(n_items / 8)
     float scale_log2;   // log2(e) / sqrt(D)
     float scale_nat;    // 1 / sqrt(D)
+    float* rho_out;     // caching step only: fp32 [B,H,T]
+    uint16_t* resid_out;  // caching step only: bf16 [B,H,T,D]
 };
 
-hipError_t launch_attention(const AttnArgs& a, int D, int block, bool reshape, hipStream_t stream);
+// What one launch computes: attention over the kept blocks (or every block when
+// dense), the same with the reshape epilogue, or the one-pass caching step
+// (every block, with the kept / not-kept split of the CSR).
+enum AttnMode { kAttn = 0, kAttnReshape = 1, kAttnCache = 2 };
+
+hipError_t launch_attention(const AttnArgs& a, int D, int block, AttnMode mode, hipStream_t stream);
 
 hipError_t launch_cache_build(const uint16_t* o_full, const float* m_full, const float* l_full,
                               const uint16_t* o_sparse, const float* m_sparse,

@@ -134,6 +134,17 @@ def test_attention_argument_errors(lib):
     ra = lib.rt_reshape_apply
     assert ra(FAKE, FAKE, FAKE, float("inf"), d, FAKE, None) == _lib.RT_EINVAL
     assert ra(FAKE, None, FAKE, 0.0, d, FAKE, None) == _lib.RT_EINVAL
+    ac = lib.rt_attn_cache
+    other = FAKE + 0x100000
+    assert ac(FAKE, FAKE, FAKE, d, ctypes.byref(b), other, None, None, None, FAKE + 0x200000, None) == _lib.RT_EINVAL
+    assert ac(FAKE, FAKE, FAKE, d, ctypes.byref(b), other, None, None, FAKE, None, None) == _lib.RT_EINVAL
+    assert ac(FAKE, FAKE, FAKE, d, ctypes.byref(b), other, None, None, FAKE, other, None) == _lib.RT_EINVAL
+    assert "alias" in lib.rt_last_error().decode()
+    assert ac(FAKE, FAKE, FAKE, d, ctypes.byref(b), FAKE, None, None, FAKE, other, None) == _lib.RT_EINVAL
+    assert ac(FAKE, FAKE, FAKE, d, ctypes.byref(_bsr(block=16)), other, None, None, FAKE, FAKE + 0x200000,
+              None) == _lib.RT_EUNSUPPORTED
+    assert ac(FAKE, FAKE, FAKE, _dims(T=1 << 24, D=72), ctypes.byref(_bsr(n_qblk=1 << 18)), other, None, None,
+              FAKE, FAKE + 0x200000, None) == _lib.RT_EINVAL
     cb = lib.rt_cache_build
     assert cb(FAKE, FAKE, FAKE, FAKE, FAKE, None, d, FAKE, FAKE, None) == _lib.RT_EINVAL
     assert cb(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, _dims(D=80), FAKE, FAKE, None) == _lib.RT_EUNSUPPORTED
@@ -147,4 +158,6 @@ def test_empty_problem_is_a_no_op(lib):
     assert lib.rt_cache_build(None, None, None, None, None, None, d, None, None, None) == _lib.RT_OK
     b = _bsr(n_qblk=0, nnz=0)
     assert lib.rt_attn_sparse(None, None, None, _dims(T=0), ctypes.byref(b), None, None, None, None) == _lib.RT_OK
+    assert lib.rt_attn_cache(None, None, None, _dims(T=0), ctypes.byref(b), None, None, None, None, None,
+                             None) == _lib.RT_OK
     assert lib.rt_last_error().decode() == ""
