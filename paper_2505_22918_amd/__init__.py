@@ -271,16 +271,15 @@ class StatCache:
     def is_caching_step(self, t):
         """Steps 0 .. full_steps-1 are full; afterwards every period-th step,
         counted from the last full step, is a full caching step."""
-        if t < self.full_steps:
-            return True
-        return self.period > 0 and (t - self.full_steps + 1) % self.period == 0
+        from .schedule import is_caching_step
+
+        return is_caching_step(t, self.full_steps, self.period)
 
     def attend(self, q, k, v, t):
-        """Attention output at denoising step t (full at caching steps)."""
+        """Attention output at denoising step t (full at caching steps, where the
+        one-pass caching kernel also refreshes rho and R)."""
         if self.is_caching_step(t) or self.rho is None:
-            o_f, m_f, l_f = attn_full(q, k, v, block=self.mask.block)
-            o_s, m_s, l_s = attn_sparse(q, k, v, self.mask)
-            self.rho, self.resid = cache_build(o_f, m_f, l_f, o_s, m_s, l_s)
+            o_f, self.rho, self.resid = attn_cache(q, k, v, self.mask, stats=False)
             self.cached_at = t
             return o_f
         delta = self.lam * (t - self.cached_at)

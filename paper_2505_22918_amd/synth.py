@@ -139,6 +139,17 @@ def make_qkv(wl: Workload, step: int = 1, seed: int | None = None):
     return tuple(out)
 
 
+def evolve_qkv(bits, sigma: float, seed: int):
+    """The next denoising step's inputs: each of Q, K, V plus sigma * N(0, 1)
+    (numpy default_rng(seed)), re-rounded to bf16.  ``bits`` are uint16 arrays."""
+    rng = np.random.default_rng(seed)
+    out = []
+    for b in bits:
+        x = bf16_bits_to_f32(b) + np.float32(sigma) * rng.standard_normal(b.shape, dtype=np.float32)
+        out.append(f32_to_bf16_bits(x))
+    return tuple(out)
+
+
 def explicit_block_mask(n_blk: int, seed: int = 0, extra: int = 1):
     """0/1 [n_blk, n_blk]: the diagonal plus ``extra`` other key blocks per row."""
     rng = np.random.default_rng(seed + 1000)
