@@ -54,18 +54,23 @@ typedef struct {
     int32_t B, H, T, D;
 } rt_dims;
 
-/* A block CSR on the device, shared by all (batch, head).
- * row_ptr [n_qblk + 1] and col_idx [nnz] are device int32 arrays.  The kernels
- * clamp row_ptr entries to [0, nnz] and skip column indices outside
- * [0, n_qblk), so a malformed CSR cannot make them read out of bounds; a query
- * block with no kept key block is outside Eq.5 (empty denominator) and its
- * rows come out as NaN. */
+/* A block CSR on the device: one mask shared by all (batch, head), or one per
+ * head, or one per (batch, head) (Eq.5 indexes the kept set by head).
+ * row_ptr [n_masks][n_qblk + 1] and col_idx [nnz] are device int32 arrays;
+ * row_ptr entries are absolute offsets into col_idx (mask m's rows start at
+ * row_ptr[m][0]).  Head h of batch b uses mask 0 (n_masks 0 or 1), mask h
+ * (n_masks == H) or mask b*H + h (n_masks == B*H).  The kernels clamp row_ptr
+ * entries to [0, nnz] and skip column indices outside [0, n_qblk), so a
+ * malformed CSR cannot make them read out of bounds; a query block with no
+ * kept key block is outside Eq.5 (empty denominator) and its rows come out as
+ * NaN (rt_attn_cache handles it: rho = 0). */
 typedef struct {
     const int32_t* row_ptr;
     const int32_t* col_idx;
-    int32_t block;  /* 32 or 64 */
-    int32_t n_qblk; /* must equal ceil(T / block) */
-    int32_t nnz;    /* entries in col_idx */
+    int32_t block;   /* 32 or 64 */
+    int32_t n_qblk;  /* must equal ceil(T / block) */
+    int32_t nnz;     /* entries in col_idx */
+    int32_t n_masks; /* 0 or 1 (shared), H or B*H */
 } rt_bsr;
 
 /* Static mask patterns (Sec.3 static masks; App. A.4 local windows). */
@@ -85,6 +90,11 @@ typedef struct {
     int32_t keep;             /* LOCAL2D: key blocks kept per query block;
                                  VIDEO3D: video key blocks kept per video query
                                  block (text key blocks are always kept)         */
+    int32_t n_masks;          /* EXPLICIT: masks stacked in mask / host_mask
+                                 (n_masks x n_qblk x n_qblk; 0 means 1); the
+                                 built CSR holds n_masks row_ptr arrays.  The
+                                 window patterns are the same for every head
+                                 and take 0 or 1.                                */
 } rt_pattern;
 
 /*
@@ -101,12 +111,14 @@ typedef struct {
  */
 
 /* Host only.  Writes the exact number of CSR entries rt_index_build produces.
- * EXPLICIT reads pattern->host_mask (host, n_qblk x n_qblk).  Needs T >= 1,
+ * EXPLICIT reads pattern->host_mask (host, n_masks x n_qblk x n_qblk).  Needs T >= 1,
  * block in {32, 64}, grid sizes matching T (LOCAL2D: grid_h*grid_w == T;
  * VIDEO3D: n_text + frames*grid_h*grid_w == T), keep >= 1, n_qblk <= 4096. */
 rt_status rt_index_size(const rt_pattern* pattern, int32_t T, int32_t block, int32_t* nnz_out);
 
-/* Builds the CSR on the device: row_ptr [ceil(T/block)+1], col_idx [capacity].
+/* Builds the CSR on the device: row_ptr [n_masks][ceil(T/block)+1] (absolute
+ * offsets), col_idx [capacity]; EXPLICIT with several masks needs
+ * n_masks * ceil(T/block) <= 32768.
  * For LOCAL2D / VIDEO3D the size is known on the host and a capacity below it
  * is RT_ECAPACITY.  EXPLICIT reads pattern->mask (device) and writes at most
  * `capacity` entries; it returns RT_ECAPACITY when pattern->host_mask is given

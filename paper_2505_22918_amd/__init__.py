@@ -82,33 +82,37 @@ def _bf16(t, shape, name):
 
 @dataclass
 class BlockMask:
-    """Block CSR on the device: row_ptr [n_qblk+1], col_idx [nnz] (int32)."""
+    """Block CSR on the device: row_ptr [n_masks][n_qblk+1] (absolute offsets),
+    col_idx [nnz] (int32).  n_masks is 1 (shared by every head), H (per head) or
+    B*H (per batch and head)."""
 
     row_ptr: object
     col_idx: object
     block: int
     n_qblk: int
     nnz: int
+    n_masks: int = 1
 
     def c_struct(self):
         return _lib.RtBsr(self.row_ptr.data_ptr(), self.col_idx.data_ptr(), self.block, self.n_qblk,
-                          self.nnz)
+                          self.nnz, self.n_masks)
 
     @classmethod
-    def from_csr(cls, row_ptr, col_idx, block, device="cuda"):
+    def from_csr(cls, row_ptr, col_idx, block, device="cuda", n_masks=1):
         """Copies a host CSR (numpy / lists) to the device as-is."""
         torch = _torch()
         rp = torch.as_tensor(row_ptr, dtype=torch.int32).to(device).contiguous()
         ci = torch.as_tensor(col_idx, dtype=torch.int32).to(device).contiguous()
-        return cls(rp, ci, int(block), int(rp.numel()) - 1, int(ci.numel()))
+        return cls(rp, ci, int(block), int(rp.numel()) // int(n_masks) - 1, int(ci.numel()), int(n_masks))
 
 
-def _pattern(kind, grid_h=0, grid_w=0, frames=0, n_text=0, keep=0, mask=None, host_mask=None):
+def _pattern(kind, grid_h=0, grid_w=0, frames=0, n_text=0, keep=0, mask=None, host_mask=None, n_masks=1):
     p = _lib.RtPattern()
     p.kind = int(kind)
     p.mask = mask.data_ptr() if mask is not None else None
     p.host_mask = host_mask.ctypes.data if host_mask is not None else None
     p.grid_h, p.grid_w, p.frames, p.n_text, p.keep = int(grid_h), int(grid_w), int(frames), int(n_text), int(keep)
+    p.n_masks = int(n_masks)
     return p
 
 
@@ -118,7 +122,8 @@ def index_size(T, block, kind, host_mask=None, **pat):
 
     lib = _lib.load()
     hm = np.ascontiguousarray(host_mask, dtype=np.uint8) if host_mask is not None else None
-    p = _pattern(kind, host_mask=hm, **pat)
+    n_masks = hm.shape[0] if hm is not None and hm.ndim == 3 else 1
+    p = _pattern(kind, host_mask=hm, n_masks=n_masks, **pat)
     out = ctypes.c_int32(0)
     _lib.check("rt_index_size", lib.rt_index_size(ctypes.byref(p), int(T), int(block), ctypes.byref(out)))
     return int(out.value)
@@ -133,21 +138,24 @@ def build_index(T, block, kind, device="cuda", host_mask=None, **pat) -> BlockMa
     n_blk = (int(T) + int(block) - 1) // int(block)
     hm = None
     dmask = None
+    n_masks = 1
     if kind == PAT_EXPLICIT:
         hm = np.ascontiguousarray(host_mask, dtype=np.uint8)
-        if hm.shape != (n_blk, n_blk):
-            raise ValueError(f"host_mask must be {n_blk}x{n_blk}")
+        if hm.ndim == 3:  # one mask per head, or per (batch, head)
+            n_masks = hm.shape[0]
+        if hm.shape[-2:] != (n_blk, n_blk) or hm.ndim not in (2, 3):
+            raise ValueError(f"host_mask must be [n_masks,] {n_blk}x{n_blk}")
         dmask = torch.from_numpy(hm).to(device)
     nnz = index_size(T, block, kind, host_mask=hm, **pat)
-    row_ptr = torch.empty(n_blk + 1, dtype=torch.int32, device=device)
+    row_ptr = torch.empty(n_masks * (n_blk + 1), dtype=torch.int32, device=device)
     col_idx = torch.empty(max(nnz, 1), dtype=torch.int32, device=device)
-    p = _pattern(kind, mask=dmask, host_mask=hm, **pat)
+    p = _pattern(kind, mask=dmask, host_mask=hm, n_masks=n_masks, **pat)
     _lib.check("rt_index_build", lib.rt_index_build(ctypes.byref(p), int(T), int(block), _ptr(row_ptr),
                                                     _ptr(col_idx), int(nnz), _stream(row_ptr)))
     if dmask is not None:
         # keep the mask alive until the build has run on the stream
         torch.cuda.current_stream(row_ptr.device).synchronize()
-    return BlockMask(row_ptr, col_idx[:nnz] if nnz else col_idx[:0], int(block), n_blk, int(nnz))
+    return BlockMask(row_ptr, col_idx[:nnz] if nnz else col_idx[:0], int(block), n_blk, int(nnz), n_masks)
 
 
 def attn_full(q, k, v, block=64, stats=True, out=None):

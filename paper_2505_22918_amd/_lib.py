@@ -33,6 +33,7 @@ class RtBsr(ctypes.Structure):
         ("block", c_int32),
         ("n_qblk", c_int32),
         ("nnz", c_int32),
+        ("n_masks", c_int32),
     ]
 
 
@@ -46,6 +47,7 @@ class RtPattern(ctypes.Structure):
         ("frames", c_int32),
         ("n_text", c_int32),
         ("keep", c_int32),
+        ("n_masks", c_int32),
     ]
 
 

@@ -115,7 +115,18 @@ rt_status check_bsr(const rt_bsr* m, const rt_dims& d) {
     if (m->nnz < 0) return fail(RT_EINVAL, "nnz=%d", m->nnz);
     if (nb > 0 && m->nnz == 0) return fail(RT_EINVAL, "empty mask: every query block needs a kept key block (Eq.5)");
     if (nb > 0 && (!m->row_ptr || !m->col_idx)) return fail(RT_EINVAL, "row_ptr / col_idx is NULL");
+    const int64_t bh = (int64_t)d.B * d.H;
+    if (m->n_masks != 0 && m->n_masks != 1 && m->n_masks != d.H && m->n_masks != bh)
+        return fail(RT_EINVAL, "n_masks=%d (need 1, H=%d or B*H=%lld)", m->n_masks, d.H, (long long)bh);
     return RT_OK;
+}
+
+void set_mask(rt::AttnArgs& a, const rt_bsr* m, const rt_dims& d) {
+    a.row_ptr = m->row_ptr;
+    a.col_idx = m->col_idx;
+    a.nnz = m->nnz;
+    a.n_masks = m->n_masks > 1 ? m->n_masks : 1;
+    a.heads = d.H;
 }
 
 int64_t lcm64(int64_t a, int64_t b) { return a / std::gcd(a, b) * b; }
@@ -134,6 +145,13 @@ rt_status pattern_args(const rt_pattern* p, int32_t T, int32_t block, rt::IndexA
     a.n_blk = (int32_t)nb;
     a.keep = p->keep;
     a.lcm = 1;
+    if (p->n_masks < 0) return fail(RT_EINVAL, "n_masks=%d", p->n_masks);
+    a.n_masks = p->n_masks > 1 ? p->n_masks : 1;
+    if (a.n_masks > 1 && p->kind != RT_PAT_EXPLICIT)
+        return fail(RT_EINVAL, "n_masks=%d: the window patterns are the same for every head", p->n_masks);
+    if (a.n_masks > 1 && (int64_t)a.n_masks * nb > 32768)
+        return fail(RT_EUNSUPPORTED, "n_masks * ceil(T/block) = %lld exceeds 32768",
+                    (long long)a.n_masks * nb);
     switch (p->kind) {
         case RT_PAT_EXPLICIT:
             *nnz = -1;
@@ -207,7 +225,7 @@ rt_status rt_index_size(const rt_pattern* pattern, int32_t T, int32_t block, int
     if (pattern->kind == RT_PAT_EXPLICIT) {
         if (!pattern->host_mask) return fail(RT_EINVAL, "EXPLICIT pattern needs host_mask for sizing");
         nnz = 0;
-        const int64_t cells = (int64_t)a.n_blk * a.n_blk;
+        const int64_t cells = (int64_t)a.n_masks * a.n_blk * a.n_blk;
         for (int64_t i = 0; i < cells; ++i) nnz += pattern->host_mask[i] != 0;
     }
     if (nnz > INT32_MAX) return fail(RT_EINVAL, "nnz exceeds int32");
@@ -266,9 +284,7 @@ rt_status rt_attn_sparse(const void* q, const void* k, const void* v, rt_dims di
     if (row_sum) RT_TRY(check_stat(row_sum, "row_sum"));
     RT_TRY(check_items(dims, mask->block));
     rt::AttnArgs a = base_args(q, k, v, dims, mask->block, o, row_max, row_sum);
-    a.row_ptr = mask->row_ptr;
-    a.col_idx = mask->col_idx;
-    a.nnz = mask->nnz;
+    set_mask(a, mask, dims);
     return hip_status(rt::launch_attention(a, dims.D, mask->block, rt::kAttn, static_cast<hipStream_t>(stream)),
                       "sparse attention launch");
 }
@@ -288,9 +304,7 @@ rt_status rt_attn_cache(const void* q, const void* k, const void* v, rt_dims dim
         return fail(RT_EINVAL, "o and resid must not alias q, k, v or each other");
     RT_TRY(check_items(dims, mask->block));
     rt::AttnArgs a = base_args(q, k, v, dims, mask->block, o, row_max, row_sum);
-    a.row_ptr = mask->row_ptr;
-    a.col_idx = mask->col_idx;
-    a.nnz = mask->nnz;
+    set_mask(a, mask, dims);
     a.rho_out = rho;
     a.resid_out = static_cast<uint16_t*>(resid);
     return hip_status(rt::launch_attention(a, dims.D, mask->block, rt::kAttnCache, static_cast<hipStream_t>(stream)),
@@ -334,9 +348,7 @@ rt_status rt_attn_sparse_reshape(const void* q, const void* k, const void* v, rt
     if (row_sum) RT_TRY(check_stat(row_sum, "row_sum"));
     RT_TRY(check_items(dims, mask->block));
     rt::AttnArgs a = base_args(q, k, v, dims, mask->block, o, row_max, row_sum);
-    a.row_ptr = mask->row_ptr;
-    a.col_idx = mask->col_idx;
-    a.nnz = mask->nnz;
+    set_mask(a, mask, dims);
     a.rho = rho;
     a.resid = static_cast<const uint16_t*>(resid);
     a.rho_delta = rho_delta;

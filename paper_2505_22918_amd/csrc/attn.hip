@@ -262,8 +262,11 @@ void attn_fwd(AttnArgs a) {
         e_beg = 0;
         e_end = a.n_blk;
     } else {
-        e_beg = ((csr_ptr)a.row_ptr)[qb];
-        e_end = ((csr_ptr)a.row_ptr)[qb + 1];
+        // the mask of this (batch, head): shared, per head, or per (batch, head)
+        const int mid = a.n_masks <= 1 ? 0 : (a.n_masks == a.heads ? bh % a.heads : bh);
+        const csr_ptr rp = (csr_ptr)a.row_ptr + (size_t)mid * (a.n_blk + 1);
+        e_beg = rp[qb];
+        e_end = rp[qb + 1];
         e_beg = e_beg < 0 ? 0 : (e_beg > a.nnz ? a.nnz : e_beg);
         e_end = e_end < e_beg ? e_beg : (e_end > a.nnz ? a.nnz : e_end);
     }

@@ -1,12 +1,13 @@
 // Block-index builder (gfx950): the static mask M of Sec.3 as a block CSR.
 //
-// Three launches on the caller's stream:
-//   1. row_count   one workgroup per query block writes its kept-block count
-//                  into row_ptr[qb + 1] (closed form for the window patterns,
-//                  a count of the 0/1 row for EXPLICIT);
-//   2. row_scan    one workgroup turns the counts into offsets in place;
-//   3. row_fill    one workgroup per query block ranks the candidate key blocks
-//                  and writes the kept ones in ascending order.
+// Three launches on the caller's stream (an EXPLICIT input may stack several
+// masks, one per head or per (batch, head); mask m owns row_ptr[m][0 .. n_blk]):
+//   1. row_count   one workgroup per (mask, query block) writes its kept-block
+//                  count into row_ptr[m][qb + 1] (closed form for the window
+//                  patterns, a count of the 0/1 row for EXPLICIT);
+//   2. row_scan    one workgroup turns all counts into absolute offsets in place;
+//   3. row_fill    one workgroup per (mask, query block) ranks the candidate key
+//                  blocks and writes the kept ones in ascending order.
 //
 // Ranking is exact integer arithmetic: a block's centroid is the sum of its
 // token coordinates scaled by lcm / count (lcm over the candidate blocks' token
@@ -25,6 +26,7 @@ namespace {
 
 constexpr int kThreads = 256;
 constexpr int kMaxBlocks = 4096;
+constexpr int kMaxRows = 32768;  // (mask, query block) rows one scan handles
 
 __device__ int row_count_of(const IndexArgs& a, int qb) {
     if (a.kind == 1) return a.keep < a.n_blk ? a.keep : a.n_blk;
@@ -37,32 +39,65 @@ __device__ int row_count_of(const IndexArgs& a, int qb) {
 }
 
 __global__ __launch_bounds__(kThreads) void row_count(IndexArgs a) {
-    const int qb = blockIdx.x;
+    const int m = blockIdx.x / a.n_blk;
+    const int qb = blockIdx.x - m * a.n_blk;
+    int32_t* const rp = a.row_ptr + (size_t)m * (a.n_blk + 1);
     __shared__ int total;
     if (a.kind != 0) {
-        if (threadIdx.x == 0) a.row_ptr[qb + 1] = row_count_of(a, qb);
+        if (threadIdx.x == 0) rp[qb + 1] = row_count_of(a, qb);
         return;
     }
     if (threadIdx.x == 0) total = 0;
     __syncthreads();
     int n = 0;
-    const uint8_t* row = a.mask + (size_t)qb * a.n_blk;
+    const uint8_t* row = a.mask + ((size_t)m * a.n_blk + qb) * a.n_blk;
     for (int kb = threadIdx.x; kb < a.n_blk; kb += kThreads) n += row[kb] != 0;
     atomicAdd(&total, n);
     __syncthreads();
-    if (threadIdx.x == 0) a.row_ptr[qb + 1] = total;
+    if (threadIdx.x == 0) rp[qb + 1] = total;
 }
 
+// Exclusive scan of the n_masks * n_blk row counts, in row order, into absolute
+// offsets: row_ptr[m][qb] = entries of all earlier rows, row_ptr[m][n_blk] =
+// row_ptr[m + 1][0] (the total after the last mask).
 __global__ __launch_bounds__(kThreads) void row_scan(IndexArgs a) {
-    __shared__ int cnt[kMaxBlocks + 1];
-    for (int i = threadIdx.x; i < a.n_blk; i += kThreads) cnt[i + 1] = a.row_ptr[i + 1];
-    __syncthreads();
-    if (threadIdx.x == 0) {
-        cnt[0] = 0;
-        for (int i = 1; i <= a.n_blk; ++i) cnt[i] += cnt[i - 1];
+    __shared__ int cnt[kMaxRows];
+    __shared__ int part[kThreads + 1];
+    const int nb = a.n_blk;
+    const int n = a.n_masks * nb;
+    const int tid = threadIdx.x;
+    for (int i = tid; i < n; i += kThreads) {
+        const int m = i / nb, qb = i - m * nb;
+        cnt[i] = a.row_ptr[(size_t)m * (nb + 1) + qb + 1];
     }
     __syncthreads();
-    for (int i = threadIdx.x; i <= a.n_blk; i += kThreads) a.row_ptr[i] = cnt[i];
+    // each thread owns a contiguous segment; segment sums are scanned serially
+    const int seg = (n + kThreads - 1) / kThreads;
+    const int s0 = tid * seg < n ? tid * seg : n;
+    const int s1 = s0 + seg < n ? s0 + seg : n;
+    int local = 0;
+    for (int i = s0; i < s1; ++i) local += cnt[i];
+    part[tid + 1] = local;
+    __syncthreads();
+    if (tid == 0) {
+        part[0] = 0;
+        for (int i = 1; i <= kThreads; ++i) part[i] += part[i - 1];
+    }
+    __syncthreads();
+    int run = part[tid];
+    for (int i = s0; i < s1; ++i) {
+        const int c = cnt[i];
+        cnt[i] = run;
+        run += c;
+    }
+    __syncthreads();
+    const int total = part[kThreads];
+    for (int i = tid; i < n; i += kThreads) {
+        const int m = i / nb, qb = i - m * nb;
+        a.row_ptr[(size_t)m * (nb + 1) + qb] = cnt[i];
+    }
+    for (int m = tid; m < a.n_masks; m += kThreads)
+        a.row_ptr[(size_t)m * (nb + 1) + nb] = m + 1 < a.n_masks ? cnt[(m + 1) * nb] : total;
 }
 
 // scaled centroid coordinates of block b (video: b holds video tokens only)
@@ -95,8 +130,9 @@ __global__ __launch_bounds__(kThreads) void row_fill(IndexArgs a) {
     __shared__ uint8_t kept[kMaxBlocks];
     __shared__ int part[kThreads + 1];
 
-    const int qb = blockIdx.x;
     const int nb = a.n_blk;
+    const int m = blockIdx.x / nb;
+    const int qb = blockIdx.x - m * nb;
     const int tid = threadIdx.x;
 
     // candidate range and how many of them to keep
@@ -138,7 +174,7 @@ __global__ __launch_bounds__(kThreads) void row_fill(IndexArgs a) {
         // text query block: text key blocks only
         for (int kb = tid; kb < nb; kb += kThreads) kept[kb] = kb < a.n_tblk;
     } else {
-        const uint8_t* row = a.mask + (size_t)qb * nb;
+        const uint8_t* row = a.mask + ((size_t)m * nb + qb) * nb;
         for (int kb = tid; kb < nb; kb += kThreads) kept[kb] = row[kb] != 0;
     }
     __syncthreads();
@@ -156,7 +192,7 @@ __global__ __launch_bounds__(kThreads) void row_fill(IndexArgs a) {
         for (int i = 1; i <= kThreads; ++i) part[i] += part[i - 1];
     }
     __syncthreads();
-    int pos = a.row_ptr[qb] + part[tid];
+    int pos = a.row_ptr[(size_t)m * (nb + 1) + qb] + part[tid];
     for (int kb = s0; kb < s1; ++kb) {
         if (kept[kb]) {
             if (pos >= 0 && pos < a.capacity) a.col_idx[pos] = kb;
@@ -168,13 +204,14 @@ __global__ __launch_bounds__(kThreads) void row_fill(IndexArgs a) {
 }  // namespace
 
 hipError_t launch_index_build(const IndexArgs& a, hipStream_t stream) {
-    hipLaunchKernelGGL(row_count, dim3(a.n_blk), dim3(kThreads), 0, stream, a);
+    const int rows = a.n_masks * a.n_blk;
+    hipLaunchKernelGGL(row_count, dim3(rows), dim3(kThreads), 0, stream, a);
     hipError_t err = hipGetLastError();
     if (err != hipSuccess) return err;
     hipLaunchKernelGGL(row_scan, dim3(1), dim3(kThreads), 0, stream, a);
     err = hipGetLastError();
     if (err != hipSuccess) return err;
-    hipLaunchKernelGGL(row_fill, dim3(a.n_blk), dim3(kThreads), 0, stream, a);
+    hipLaunchKernelGGL(row_fill, dim3(rows), dim3(kThreads), 0, stream, a);
     return hipGetLastError();
 }
 

@@ -17,9 +17,11 @@ struct AttnArgs {
     const float* rho;   // reshape only: fp32 [B,H,T]
     const uint16_t* resid;  // reshape only: bf16 [B,H,T,D]
     float rho_delta;
-    const int32_t* row_ptr;  // sparse only
+    const int32_t* row_ptr;  // sparse only: [n_masks][n_blk + 1], absolute offsets
     const int32_t* col_idx;
     int32_t nnz;
+    int32_t n_masks;    // 1: shared; H: per head; B*H: per (batch, head)
+    int32_t heads;      // H
     int32_t T;
     int32_t n_blk;      // ceil(T / block)
     int32_t dense;      // 1: walk every key block, ignore the CSR
@@ -53,6 +55,7 @@ struct IndexArgs {
     int32_t T, block, n_blk;
     int32_t grid_h, grid_w, frames, n_text;
     int32_t keep;
+    int32_t n_masks;      // EXPLICIT masks stacked in `mask`
     int32_t n_tblk;       // VIDEO3D text blocks
     int64_t lcm;          // lcm of candidate block token counts
     int32_t* row_ptr;

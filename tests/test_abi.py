@@ -71,6 +71,7 @@ def _pat(**kw):
     p.frames = kw.get("frames", 0)
     p.n_text = kw.get("n_text", 0)
     p.keep = kw.get("keep", 1)
+    p.n_masks = kw.get("n_masks", 0)
     return p
 
 
@@ -148,6 +149,32 @@ def test_attention_argument_errors(lib):
     cb = lib.rt_cache_build
     assert cb(FAKE, FAKE, FAKE, FAKE, FAKE, None, d, FAKE, FAKE, None) == _lib.RT_EINVAL
     assert cb(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, _dims(D=80), FAKE, FAKE, None) == _lib.RT_EUNSUPPORTED
+
+
+def test_mask_count_errors(lib):
+    d = _dims(B=2, H=3)
+    st = lib.rt_attn_sparse
+    for bad in (2, 4, 5, -1):
+        b = _lib.RtBsr(FAKE, FAKE, 64, 4, 8, bad)
+        assert st(FAKE, FAKE, FAKE, d, ctypes.byref(b), FAKE, None, None, None) == _lib.RT_EINVAL
+        assert "n_masks" in lib.rt_last_error().decode()
+    n = ctypes.c_int32(0)
+    # several masks only for EXPLICIT; bounded rows for the scan
+    assert lib.rt_index_size(ctypes.byref(_pat(n_masks=3)), 64, 64, ctypes.byref(n)) == _lib.RT_EINVAL
+    p = _pat(kind=0, n_masks=16)
+    hm = np.ones((16, 4096, 1), np.uint8)
+    p.host_mask = hm.ctypes.data
+    assert lib.rt_index_size(ctypes.byref(p), 4096 * 32, 32, ctypes.byref(n)) in (_lib.RT_EUNSUPPORTED,)
+
+
+def test_index_size_counts_every_stacked_mask(lib):
+    import paper_2505_22918_amd as rt
+    from paper_2505_22918_amd import synth
+
+    nb = 5
+    masks = np.stack([synth.explicit_block_mask(nb, seed=s) for s in range(3)])
+    masks[1, 2, :] = 1
+    assert rt.index_size(nb * 64, 64, synth.PAT_EXPLICIT, host_mask=masks) == int(masks.sum())
 
 
 def test_empty_problem_is_a_no_op(lib):
