@@ -156,6 +156,15 @@ rt_status rt_attn_sparse(const void* q, const void* k, const void* v, rt_dims di
 rt_status rt_attn_cache(const void* q, const void* k, const void* v, rt_dims dims, const rt_bsr* mask,
                         void* o, float* row_max, float* row_sum, float* rho, void* resid, void* stream);
 
+/* Post-softmax masking, Eq.7 (the Sec.3 toy operation, an ablation, not a
+ * speedup): O = (A o M) V, the full softmax A of Eq.4 with the masked entries
+ * zeroed and the full denominator kept, so each row sums to rho < 1.  Runs the
+ * caching walk (every key block) and writes only o: device bf16 [B,H,T,D]
+ * (must not alias q, k, v).  Equals rho * SparseAttention(Q,K,V) of the same
+ * step (Eq.8). */
+rt_status rt_attn_postmask(const void* q, const void* k, const void* v, rt_dims dims, const rt_bsr* mask,
+                           void* o, void* stream);
+
 /* Statistics cache at a caching (full-attention) step, Eq.8 and Eq.10:
  *   rho = (l_sparse / l_full) * exp(m_sparse - m_full)      (Eq.8)
  *   R   = O_full - rho * O_sparse                           (Eq.10)

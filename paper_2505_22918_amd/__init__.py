@@ -28,6 +28,7 @@ __all__ = [
     "attn_full",
     "attn_sparse",
     "attn_cache",
+    "attn_postmask",
     "cache_build",
     "attn_sparse_reshape",
     "reshape_apply",
@@ -206,6 +207,18 @@ def attn_cache(q, k, v, mask: BlockMask, stats=True, out=None):
     _lib.check("rt_attn_cache", lib.rt_attn_cache(_ptr(q), _ptr(k), _ptr(v), dims, ctypes.byref(bsr), _ptr(o),
                                                   _ptr(m), _ptr(l), _ptr(rho), _ptr(resid), _stream(q)))
     return (o, rho, resid, m, l) if stats else (o, rho, resid)
+
+
+def attn_postmask(q, k, v, mask: BlockMask, out=None):
+    """Post-softmax masking (Eq.7): (A o M) V with the full denominator."""
+    torch = _torch()
+    lib = _lib.load()
+    dims = _check_qkv(q, k, v)
+    o = out if out is not None else torch.empty_like(q)
+    bsr = mask.c_struct()
+    _lib.check("rt_attn_postmask", lib.rt_attn_postmask(_ptr(q), _ptr(k), _ptr(v), dims, ctypes.byref(bsr),
+                                                        _ptr(o), _stream(q)))
+    return o
 
 
 def cache_build(o_full, m_full, l_full, o_sparse, m_sparse, l_sparse):

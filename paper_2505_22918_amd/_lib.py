@@ -61,6 +61,8 @@ _SIGS = {
                                  c_void_p, c_void_p, c_void_p, c_void_p]),
     "rt_attn_cache": (c_int32, [c_void_p, c_void_p, c_void_p, RtDims, ctypes.POINTER(RtBsr), c_void_p,
                                 c_void_p, c_void_p, c_void_p, c_void_p, c_void_p]),
+    "rt_attn_postmask": (c_int32, [c_void_p, c_void_p, c_void_p, RtDims, ctypes.POINTER(RtBsr), c_void_p,
+                                   c_void_p]),
     "rt_cache_build": (c_int32, [c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, RtDims,
                                  c_void_p, c_void_p, c_void_p]),
     "rt_attn_sparse_reshape": (c_int32, [c_void_p, c_void_p, c_void_p, RtDims, ctypes.POINTER(RtBsr),

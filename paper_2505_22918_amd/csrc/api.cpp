@@ -311,6 +311,22 @@ rt_status rt_attn_cache(const void* q, const void* k, const void* v, rt_dims dim
                       "caching-step launch");
 }
 
+rt_status rt_attn_postmask(const void* q, const void* k, const void* v, rt_dims dims, const rt_bsr* mask, void* o,
+                           void* stream) {
+    bool empty = false;
+    RT_TRY(check_dims(dims, &empty));
+    RT_TRY(check_bsr(mask, dims));
+    if (empty) return ok();
+    RT_TRY(check_qkv(q, k, v, o));
+    if (o == q || o == k || o == v) return fail(RT_EINVAL, "o must not alias q, k or v");
+    RT_TRY(check_items(dims, mask->block));
+    rt::AttnArgs a = base_args(q, k, v, dims, mask->block, o, nullptr, nullptr);
+    set_mask(a, mask, dims);
+    a.postmask = 1;
+    return hip_status(rt::launch_attention(a, dims.D, mask->block, rt::kAttnCache, static_cast<hipStream_t>(stream)),
+                      "post-softmax masking launch");
+}
+
 rt_status rt_cache_build(const void* o_full, const float* m_full, const float* l_full, const void* o_sparse,
                          const float* m_sparse, const float* l_sparse, rt_dims dims, float* rho, void* resid,
                          void* stream) {

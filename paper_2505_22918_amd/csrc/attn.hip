@@ -745,7 +745,7 @@ void attn_fwd(AttnArgs a) {
             const float lf = li + lo;
             const float inv = 1.0f / lf;
             const float rho = split ? li / lf : 1.0f;  // exactly 1 when every block is kept
-            if (hi == 0 && row < T) {
+            if (hi == 0 && row < T && !a.postmask) {
                 const size_t si = (size_t)bh * T + row;
                 a.rho_out[si] = rho;
                 if (STATS) {
@@ -766,12 +766,18 @@ void attn_fwd(AttnArgs a) {
                             const float acc = oacc[qt][dt][8 * u + e] * inv;
                             const float osv = (e & 1) ? hi_f(os4[e >> 1]) : lo_f(os4[e >> 1]);
                             r[e] = split ? acc : 0.f;
-                            of[e] = split ? __builtin_fmaf(rho, osv, acc) : acc;
+                            if (a.postmask) {  // Eq.7: (A o M) V = rho O_s
+                                of[e] = split ? rho * osv : acc;
+                            } else {
+                                of[e] = split ? __builtin_fmaf(rho, osv, acc) : acc;
+                            }
                         }
                         const size_t off = head_off + (size_t)row * D + 8 * ch;
-                        *reinterpret_cast<u32x4*>(a.resid_out + off) =
-                            u32x4{pack_bf16(r[0], r[1]), pack_bf16(r[2], r[3]), pack_bf16(r[4], r[5]),
-                                  pack_bf16(r[6], r[7])};
+                        if (!a.postmask) {
+                            *reinterpret_cast<u32x4*>(a.resid_out + off) =
+                                u32x4{pack_bf16(r[0], r[1]), pack_bf16(r[2], r[3]), pack_bf16(r[4], r[5]),
+                                      pack_bf16(r[6], r[7])};
+                        }
                         *reinterpret_cast<u32x4*>(a.o + off) = u32x4{pack_bf16(of[0], of[1]), pack_bf16(of[2], of[3]),
                                                                      pack_bf16(of[4], of[5]), pack_bf16(of[6], of[7])};
                     }

@@ -31,6 +31,7 @@ struct AttnArgs {
     float scale_nat;    // 1 / sqrt(D)
     float* rho_out;     // caching step only: fp32 [B,H,T]
     uint16_t* resid_out;  // caching step only: bf16 [B,H,T,D]
+    int32_t postmask;   // caching walk only: write (A o M) V (Eq.7) to o instead of O_full, rho, R
 };
 
 // What one launch computes: attention over the kept blocks (or every block when

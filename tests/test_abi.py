@@ -146,6 +146,10 @@ def test_attention_argument_errors(lib):
               None) == _lib.RT_EUNSUPPORTED
     assert ac(FAKE, FAKE, FAKE, _dims(T=1 << 24, D=72), ctypes.byref(_bsr(n_qblk=1 << 18)), other, None, None,
               FAKE, FAKE + 0x200000, None) == _lib.RT_EINVAL
+    pm = lib.rt_attn_postmask
+    assert pm(FAKE, FAKE, FAKE, d, ctypes.byref(b), FAKE, None) == _lib.RT_EINVAL  # o aliases q
+    assert pm(FAKE, FAKE, FAKE, d, ctypes.byref(b), None, None) == _lib.RT_EINVAL
+    assert pm(FAKE, FAKE, FAKE, d, None, FAKE + 0x100000, None) == _lib.RT_EINVAL
     cb = lib.rt_cache_build
     assert cb(FAKE, FAKE, FAKE, FAKE, FAKE, None, d, FAKE, FAKE, None) == _lib.RT_EINVAL
     assert cb(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, _dims(D=80), FAKE, FAKE, None) == _lib.RT_EUNSUPPORTED

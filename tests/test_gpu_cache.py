@@ -159,3 +159,45 @@ def test_cache_step_workload_rows(gpu, name):
     assert_stat_close(cat(got, "rho"), cat(ref, "rho"), f"{name} rho")
     assert np.all(np.isfinite(g["o"])) and np.all(np.isfinite(g["resid"]))
     assert g["rho"].min() > 0.0 and g["rho"].max() <= 1.0 + 1e-6
+
+
+def test_post_softmax_masking(gpu):
+    """Eq.7: (A o M) V keeps the full denominator, so it equals the brute-force
+    masked matrix times V, equals rho * O_s (Eq.8), and with V = 1 every row
+    comes out as its rho."""
+    import torch
+
+    T, D, block = 256, 64, 64
+    print("[cache] post-softmax masking", flush=True)
+    s1, _ = _inputs(1, 1, T, D, seed=13)
+    nb = ob.n_blocks(T, block)
+    hm = synth.explicit_block_mask(nb, seed=5)
+    mask = rt.build_index(T, block, synth.PAT_EXPLICIT, host_mask=hm)
+    q, k, v = (to_dev(x) for x in s1)
+    o_post = rt.attn_postmask(q, k, v, mask)
+    ones = torch.ones_like(v)
+    o_ones = rt.attn_postmask(q, k, ones, mask)
+    _, rho, _ = rt.attn_cache(q, k, v, mask, stats=False)
+    torch.cuda.synchronize()
+    Q, K, V = (f64(x) for x in s1)
+    orp, oci = ob.block_index_explicit(hm)
+    bf = oa.brute_force(Q[0, 0], K[0, 0], V[0, 0], ob.token_mask(orp, oci, block, T), 0.0)
+    assert_bf16_close(to_np(o_post)[0, 0], bf["o_post"], "(A o M) V")
+    assert_bf16_close(to_np(o_post)[0, 0], bf["rho"][:, None] * bf["o_sparse"], "rho O_s")
+    # rows of A o M sum to rho: with V = 1 each output element is its row's rho
+    np.testing.assert_allclose(to_np(o_ones)[0, 0], np.repeat(to_np(rho)[0, 0][:, None], D, axis=1),
+                               rtol=2 ** -8, atol=0)
+    np.testing.assert_allclose(to_np(rho)[0, 0], bf["rho"], rtol=1e-3, atol=0)
+
+    for case in CASES[1:4]:
+        name, B, H, T2, D2, block2, pat = case
+        s, _ = _inputs(B, H, T2, D2, seed=zlib.crc32(name.encode()) % 1000 + 1)
+        m2, (rp2, ci2) = _mask(T2, block2, pat)
+        q2, k2, v2 = (to_dev(x) for x in s)
+        got = rt.attn_postmask(q2, k2, v2, m2)
+        torch.cuda.synchronize()
+        Q2, K2, V2 = (f64(x) for x in s)
+        Of, Mf, Lf = oa.full_attention(Q2, K2, V2)
+        Os, Ms, Ls = oa.sparse_attention(Q2, K2, V2, rp2, ci2, block2)
+        Rho = oa.rho(Ms, Ls, Mf, Lf)
+        assert_bf16_close(to_np(got), Rho[..., None] * Os, f"{name} (A o M) V")
