@@ -45,8 +45,9 @@ rt_status check_dims(const rt_dims& d, bool* empty) {
     const int64_t rows = (int64_t)d.B * d.H * d.T;
     if (rows * d.D >= (int64_t)1 << 40) return fail(RT_EINVAL, "tensor too large");
     if ((int64_t)d.B * d.H >= (int64_t)1 << 24) return fail(RT_EINVAL, "B*H too large");
-    // buffer record counts and offsets within one head are 32-bit
-    if ((int64_t)d.T * d.D * 2 >= (int64_t)1 << 31) return fail(RT_EINVAL, "T=%d too long for one head", d.T);
+    // buffer record counts and offsets within one head are 32-bit, with 2^30
+    // kept free as the out-of-range offset that reads zeros
+    if ((int64_t)d.T * d.D * 2 > (int64_t)1 << 30) return fail(RT_EINVAL, "T=%d too long for one head", d.T);
     *empty = rows == 0;
     return RT_OK;
 }

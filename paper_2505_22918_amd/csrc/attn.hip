@@ -287,9 +287,28 @@ void attn_fwd(AttnArgs a) {
         return j < 64 ? __builtin_amdgcn_readlane(cols, j) : ((csr_ptr)a.col_idx)[e_beg + j];
     };
     int gen_kb = -1, gen_e = 0;  // complement walk: last block emitted, next kept entry
+    // Key bases of 64 consecutive chunks, one per lane (-1: no key), so a step
+    // reads its chunk's base with one v_readlane instead of a scalar lookup.
+    // Used for the dense walk and for CSR rows of at most 64 entries (whose
+    // column indices all sit in `cols`); the caching walk keeps the scalar path.
+    const bool use_tab = !CACHE && (a.dense || e_end - e_beg <= 64);
+    int tab = -1;
+    auto fill_tab = [&](int i0) {
+        const int i = i0 + lane;
+        const int j = i / (BS / 32), half = i - j * (BS / 32);
+        int kb = a.dense ? j : __builtin_amdgcn_ds_bpermute((j & 63) << 2, cols);
+        const int base = kb * BS + 32 * half;
+        tab = (i < n_chunk && kb >= 0 && kb < a.n_blk && base < T) ? base : -1;
+    };
+    if (use_tab) fill_tab(0);
     // Key base of chunk i, or -1 for a chunk holding no key.  Called for
-    // i = 0, 1, 2, ... in order, once each (the complement walk relies on it).
+    // i = 0, 1, 2, ... in order, once each (the table refill and the complement
+    // walk rely on it).
     auto chunk_base = [&](int i) -> int {
+        if (use_tab) {
+            if ((i & 63) == 0 && i > 0) fill_tab(i);
+            return __builtin_amdgcn_readlane(tab, i & 63);
+        }
         int kb, half;
         if (CACHE && i >= n_in) {
             const int jc = (i - n_in) / (BS / 32);
@@ -324,25 +343,21 @@ void attn_fwd(AttnArgs a) {
     auto k_off = [&](int st) { return st * TILE; };
     auto v_off = [&](int st) { return (3 + st) * TILE; };
 
-    // DMA of the 32-key chunk of `head` starting at key `base` to LDS byte offset
-    // `dst`; the buffer ends at row T, so rows past it read as zeros.  A chunk that
-    // holds no key (base < 0) gets an empty buffer: its loads read zeros and touch
-    // no memory.  Every call issues NDMA loads, so all waits below are constants.
-    auto issue = [&](const uint16_t* head, const int (&off)[NDMA], int base, int dst) {
-        const uint16_t* src = head;
-        int nrec = 0;
-        if (base >= 0) {
-            const int left = (T - base) * (D * 2);
-            nrec = left < 32 * D * 2 ? left : 32 * D * 2;
-            src = head + (size_t)base * D;
-        }
-        const i32x4 rs = buffer_rsrc(src, nrec);
+    // DMA of the 32-key chunk starting at key `base` of a head's K or V (buffer
+    // resource `rs`: the whole head, T rows) to LDS byte offset `dst`.  Rows past
+    // T fall outside the buffer and read as zeros; a chunk that holds no key
+    // (base < 0) is pointed past the buffer, so its loads read zeros and touch no
+    // memory.  Every call issues NDMA loads, so all waits below are constants.
+    const i32x4 k_rs = buffer_rsrc(Kh, T * D * 2);
+    const i32x4 v_rs = buffer_rsrc(Vh, T * D * 2);
+    auto issue = [&](const i32x4& rs, const int (&off)[NDMA], int base, int dst) {
+        const int boff = base >= 0 ? base * (D * 2) : kOob;
         if (NSLOT == 4 * 64) {
-            dma16x4(lds0 + dst, off[0], rs);
+            dma16x4(lds0 + dst, off[0] + boff, rs);
         } else {
 #pragma unroll
             for (int n = 0; n < NDMA; ++n) {
-                if (NSLOT % 64 == 0 || n * 64 + lane < NSLOT) dma16(lds0 + dst + n * 1024, off[n], rs);
+                if (NSLOT % 64 == 0 || n * 64 + lane < NSLOT) dma16(lds0 + dst + n * 1024, off[n] + boff, rs);
             }
         }
     };
@@ -389,10 +404,10 @@ void attn_fwd(AttnArgs a) {
     // issue order Q, K(0), V(0), K(1), K(2); afterwards each step issues V(t) then
     // K(t+3), so waiting for V(t-1) in step t leaves exactly three chunk loads
     // (K(t+2), V(t), K(t+3)) in flight
-    issue(Kh, kdma, c0, k_off(0));
-    issue(Vh, vdma, c0, v_off(0));
-    issue(Kh, kdma, c1, k_off(1));
-    issue(Kh, kdma, c2b, k_off(2));
+    issue(k_rs, kdma, c0, k_off(0));
+    issue(v_rs, vdma, c0, v_off(0));
+    issue(k_rs, kdma, c1, k_off(1));
+    issue(k_rs, kdma, c2b, k_off(2));
     wait_vm<3 * NDMA>();  // Q and K(0) have landed
     if (RESHAPE && n_chunk == 0) issue_resid();
     bf16x8 qop[QT][DS];
@@ -567,10 +582,10 @@ void attn_fwd(AttnArgs a) {
         const int vst = t & 1;                // stage of V(t)
         const int kn = k3 == 2 ? 0 : k3 + 1;  // stage of K(t+1)
         int cn3 = -1;
-        if (t > 0) issue(Vh, vdma, b_t, v_off(vst));  // V(t-2) was read in step t-1
+        if (t > 0) issue(v_rs, vdma, b_t, v_off(vst));  // V(t-2) was read in step t-1
         if (HAS_QK) {
             cn3 = t + 3 < n_chunk ? chunk_base(t + 3) : -1;
-            issue(Kh, kdma, cn3, k_off(k3));  // K(t) was read in step t-1
+            issue(k_rs, kdma, cn3, k_off(k3));  // K(t) was read in step t-1
         }
         if (HAS_QK && HAS_PV) {
             wait_vm<3 * NDMA>();  // K(t+2), V(t), K(t+3) may still fly

@@ -118,7 +118,9 @@ def test_two_step_pipeline_matches_oracle(gpu, case):
 def test_density_one_sparse_is_full_bitwise(gpu):
     import torch
 
-    for (T, D, block) in [(300, 64, 64), (200, 72, 32)]:
+    # 80 key blocks: rows past 64 entries take the scalar CSR lookup, the dense
+    # walk the per-lane table (refilled every 64 chunks); both must agree bitwise
+    for (T, D, block) in [(300, 64, 64), (200, 72, 32), (80 * 64, 64, 64)]:
         print(f"[attn] density-1 T={T} D={D} block={block}", flush=True)
         s1, _ = _inputs(1, 2, T, D, seed=5)
         q, k, v = (to_dev(x) for x in s1)
