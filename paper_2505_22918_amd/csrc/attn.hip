@@ -23,7 +23,7 @@
 // Memory.  Q arrives by buffer loads straight into its B-operand registers.
 // K and V chunks move from HBM/L2 into LDS rings (three K stages, two V stages,
 // 20 KB per wave at D = 64) with buffer_load ... lds (no staging registers);
-// K(t+2), K(t+3) and V(t) are in flight while chunk t is softmaxed.  Buffer
+// K(t+2), K(t+3) and V(t+1) are in flight while chunk t is softmaxed.  Buffer
 // resources end at the last key row, so rows past T arrive as zeros (their
 // scores are then masked).
 // Rows stay row-major in LDS: K is read as the A operand with 16-byte reads,
@@ -31,9 +31,10 @@
 // of a row are XOR-swizzled by row so both reads are free of bank conflicts
 // (72-wide heads use 144-byte rows, which spread banks as is).
 //
-// Software pipeline.  Step t issues the DMA of V(t) and K(t+3), then runs the
-// P V product of chunk t-1 on the matrix cores under the exponentials of chunk
-// t's softmax, packs chunk t's probabilities to bf16 in the registers P V(t-1)
+// Software pipeline.  Step t issues the DMA of K(t+3), runs the P V product of
+// chunk t-1 on the matrix cores under the exponentials of chunk t's softmax,
+// issues the DMA of V(t+1) into the stage V(t-1) has just left, packs chunk t's
+// probabilities to bf16 in the registers P V(t-1)
 // has just read, and computes S(t+1) = K Q^T into the registers softmax(t) has
 // just read (no register copies between steps).  The last step has no S
 // product; the residual loads are issued there.
@@ -401,9 +402,9 @@ void attn_fwd(AttnArgs a) {
     const int c0 = n_chunk > 0 ? chunk_base(0) : -1;
     const int c1 = n_chunk > 1 ? chunk_base(1) : -1;
     const int c2b = n_chunk > 2 ? chunk_base(2) : -1;
-    // issue order Q, K(0), V(0), K(1), K(2); afterwards each step issues V(t) then
-    // K(t+3), so waiting for V(t-1) in step t leaves exactly three chunk loads
-    // (K(t+2), V(t), K(t+3)) in flight
+    // issue order Q, K(0), V(0), K(1), K(2); afterwards step t issues K(t+3) at its
+    // start and V(t+1) after its P V product, so waiting for V(t-1) at the start of
+    // step t leaves exactly three chunk loads (K(t+2), V(t), K(t+3)) in flight
     issue(k_rs, kdma, c0, k_off(0));
     issue(v_rs, vdma, c0, v_off(0));
     issue(k_rs, kdma, c1, k_off(1));
@@ -567,10 +568,10 @@ void attn_fwd(AttnArgs a) {
     int b_t = c0, b_t1 = c1, b_t2 = c2b;
     int k3 = 0;
 
-    // Step t: issue V(t) (t > 0; V(0) left with the prologue) and K(t+3) (HAS_QK),
-    // and wait for K(t+1) and V(t-1).  Then
+    // Step t: issue K(t+3) (HAS_QK) and wait for K(t+1) and V(t-1).  Then
     //   A: P V(t-1) (HAS_PV) on the matrix cores, interleaved with the
-    //      exponentials and row sums of softmax(t) in fp32;
+    //      exponentials and row sums of softmax(t) in fp32; then the DMA of
+    //      V(t+1) into the stage V(t-1) occupied;
     //   the rare rescale (a probability reached 2^64: O and l move to the new
     //      max, chunk t is recomputed; P V(t-1) is in O by then);
     //   B: chunk t's bf16 probabilities into pk (P V(t-1) has read it), then
@@ -582,7 +583,6 @@ void attn_fwd(AttnArgs a) {
         const int vst = t & 1;                // stage of V(t)
         const int kn = k3 == 2 ? 0 : k3 + 1;  // stage of K(t+1)
         int cn3 = -1;
-        if (t > 0) issue(v_rs, vdma, b_t, v_off(vst));  // V(t-2) was read in step t-1
         if (HAS_QK) {
             cn3 = t + 3 < n_chunk ? chunk_base(t + 3) : -1;
             issue(k_rs, kdma, cn3, k_off(k3));  // K(t) was read in step t-1
@@ -643,6 +643,9 @@ void attn_fwd(AttnArgs a) {
             }
             __builtin_amdgcn_sched_barrier(0);
         }
+        // V(t+1) into the stage P V(t-1) has just read: V gets a step and a half of
+        // lead instead of one
+        if (t + 1 < n_chunk) issue(v_rs, vdma, b_t1, v_off(vst ^ 1));
         if (CACHE && t == n_in && t > 0) flush_kept();  // P V of chunk n_in - 1 is in O
         float lsum[QT];
         bool jump = false;
