@@ -483,17 +483,38 @@ void attn_fwd(AttnArgs a) {
             }
         }
     };
+    // Row sums.  Where l only normalises O (no statistics, no caching split), l
+    // sums the bf16 probabilities that P V multiplies, two per v_dot2_f32_bf16 on
+    // the packed operands; numerator and denominator then use the same weights.
+    // Where l, m or rho are outputs, l sums the fp32 probabilities.
+    constexpr bool BF16_SUM = !STATS && !CACHE;
     // fp32 probabilities of scores x0 .. x0+3 against the running max (mc = m * c2);
-    // their sum starts (first) or joins acc
+    // their sum starts (first) or joins acc (fp32 row sums only)
     auto exps4 = [&](const f32x16& sc, int x0, float mc, float* p, float& acc, bool first) {
 #pragma unroll
         for (int x = 0; x < 4; ++x) p[x] = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[x0 + x], c2, -mc));
-        const float part = (p[0] + p[1]) + (p[2] + p[3]);
-        acc = first ? part : acc + part;
+        if (!BF16_SUM) {
+            const float part = (p[0] + p[1]) + (p[2] + p[3]);
+            acc = first ? part : acc + part;
+        }
+    };
+    // sum of the 16 bf16 probabilities packed in pk (two partial chains)
+    auto bf16_sum = [&](const bf16x8 (&pk)[2]) -> float {
+        const bf16x2 one2 = {(__bf16)1.0f, (__bf16)1.0f};
+        float a0 = 0.f, a1 = 0.f;
+        a0 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pk[0], pk[0], 0, 1), one2, a0, false);
+        a1 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pk[1], pk[1], 0, 1), one2, a1, false);
+        a0 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pk[0], pk[0], 2, 3), one2, a0, false);
+        a1 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pk[1], pk[1], 2, 3), one2, a1, false);
+        a0 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pk[0], pk[0], 4, 5), one2, a0, false);
+        a1 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pk[1], pk[1], 4, 5), one2, a1, false);
+        a0 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pk[0], pk[0], 6, 7), one2, a0, false);
+        a1 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pk[1], pk[1], 6, 7), one2, a1, false);
+        return a0 + a1;
     };
     // all 16 probabilities of tile qt; returns their sum
     auto exps16 = [&](const f32x16& sc, float mc, float (&p)[16]) -> float {
-        float s0, s1;
+        float s0 = 0.f, s1 = 0.f;
         exps4(sc, 0, mc, p + 0, s0, true);
         exps4(sc, 4, mc, p + 4, s1, true);
         exps4(sc, 8, mc, p + 8, s0, false);
@@ -647,11 +668,17 @@ void attn_fwd(AttnArgs a) {
         // lead instead of one
         if (t + 1 < n_chunk) issue(v_rs, vdma, b_t1, v_off(vst ^ 1));
         if (CACHE && t == n_in && t > 0) flush_kept();  // P V of chunk n_in - 1 is in O
+        // chunk t's bf16 probabilities into pk (P V(t-1) has read it) and the row sums
         float lsum[QT];
         bool jump = false;
 #pragma unroll
         for (int qt = 0; qt < QT; ++qt) {
-            lsum[qt] = sa[qt] + sb[qt];
+            if (BF16_SUM) {
+                pack16(pf[qt], pk[qt]);
+                lsum[qt] = bf16_sum(pk[qt]);
+            } else {
+                lsum[qt] = sa[qt] + sb[qt];
+            }
             jump |= !(lsum[qt] < kJump);
         }
         if (__builtin_amdgcn_ballot_w64(jump)) {
@@ -666,13 +693,17 @@ void attn_fwd(AttnArgs a) {
                 for (int dt = 0; dt < DT; ++dt) oacc[qt][dt] *= alpha;
                 m_run[qt] = mnew;
                 lsum[qt] = exps16(s[qt], mnew * c2, pf[qt]);
+                if (BF16_SUM) {
+                    pack16(pf[qt], pk[qt]);
+                    lsum[qt] = bf16_sum(pk[qt]);
+                }
             }
         }
         // B
 #pragma unroll
         for (int qt = 0; qt < QT; ++qt) {
             l_run[qt] += lsum[qt];
-            pack16(pf[qt], pk[qt]);
+            if (!BF16_SUM) pack16(pf[qt], pk[qt]);
         }
         if (HAS_QK) {
 #pragma unroll
