@@ -668,13 +668,22 @@ void attn_fwd(AttnArgs a) {
         // lead instead of one
         if (t + 1 < n_chunk) issue(v_rs, vdma, b_t1, v_off(vst ^ 1));
         if (CACHE && t == n_in && t > 0) flush_kept();  // P V of chunk n_in - 1 is in O
-        // chunk t's bf16 probabilities into pk (P V(t-1) has read it) and the row sums
+        // Chunk t's bf16 probabilities into pk (P V(t-1) has read it) and the row
+        // sums.  With bf16 row sums the S(t+1) product is issued here, between the
+        // packs and the sums of the two tiles, rather than after the rescale test.
+        constexpr bool QK_EARLY = BF16_SUM && HAS_QK;
         float lsum[QT];
         bool jump = false;
 #pragma unroll
         for (int qt = 0; qt < QT; ++qt) {
             if (BF16_SUM) {
                 pack16(pf[qt], pk[qt]);
+                if (QK_EARLY) {
+#pragma unroll
+                    for (int ss = 0; ss < DS; ++ss)
+                        s[qt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kop[ss], qop[qt][ss], ss == 0 ? f32x16{} : s[qt],
+                                                                        0, 0, 0);
+                }
                 lsum[qt] = bf16_sum(pk[qt]);
             } else {
                 lsum[qt] = sa[qt] + sb[qt];
@@ -682,9 +691,37 @@ void attn_fwd(AttnArgs a) {
             jump |= !(lsum[qt] < kJump);
         }
         if (__builtin_amdgcn_ballot_w64(jump)) {
+            // chunk t's scores
+            f32x16 st[QT];
+            if (QK_EARLY) {
+                // s holds S(t+1) and K(t)'s stage holds K(t+3) by now: reload the
+                // lane's K(t) row from memory and form S(t) again (same operands,
+                // same products)
+                u32x4 kr[DS];
+#pragma unroll
+                for (int ss = 0; ss < DS; ++ss) {
+                    const int ch = 2 * ss + hi;
+                    kr[ss] = vload16(b_t >= 0 && ch < DC ? (b_t + l32) * (D * 2) + ch * 16 : kOob, k_rs);
+                }
+                wait_vm<0>();
+#pragma unroll
+                for (int qt = 0; qt < QT; ++qt) {
+                    st[qt] = f32x16{};
+#pragma unroll
+                    for (int ss = 0; ss < DS; ++ss) {
+                        settle(kr[ss]);
+                        st[qt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, kr[ss]), qop[qt][ss],
+                                                                         st[qt], 0, 0, 0);
+                    }
+                }
+                mask(b_t, st);
+            } else {
+#pragma unroll
+                for (int qt = 0; qt < QT; ++qt) st[qt] = s[qt];
+            }
 #pragma unroll
             for (int qt = 0; qt < QT; ++qt) {
-                if (!STATS) mx[qt] = chunk_max(s[qt]);
+                if (!STATS) mx[qt] = chunk_max(st[qt]);
                 const float mnew = fmaxf(m_run[qt], mx[qt]);
                 const float alpha = __builtin_amdgcn_exp2f((m_run[qt] - mnew) * c2);
                 l_run[qt] *= alpha;
@@ -692,7 +729,7 @@ void attn_fwd(AttnArgs a) {
 #pragma unroll
                 for (int dt = 0; dt < DT; ++dt) oacc[qt][dt] *= alpha;
                 m_run[qt] = mnew;
-                lsum[qt] = exps16(s[qt], mnew * c2, pf[qt]);
+                lsum[qt] = exps16(st[qt], mnew * c2, pf[qt]);
                 if (BF16_SUM) {
                     pack16(pf[qt], pk[qt]);
                     lsum[qt] = bf16_sum(pk[qt]);
@@ -706,12 +743,14 @@ void attn_fwd(AttnArgs a) {
             if (!BF16_SUM) pack16(pf[qt], pk[qt]);
         }
         if (HAS_QK) {
+            if (!QK_EARLY) {
 #pragma unroll
-            for (int ss = 0; ss < DS; ++ss) {
+                for (int ss = 0; ss < DS; ++ss) {
 #pragma unroll
-                for (int qt = 0; qt < QT; ++qt)
-                    s[qt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kop[ss], qop[qt][ss], ss == 0 ? f32x16{} : s[qt], 0, 0,
-                                                                    0);
+                    for (int qt = 0; qt < QT; ++qt)
+                        s[qt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kop[ss], qop[qt][ss], ss == 0 ? f32x16{} : s[qt],
+                                                                        0, 0, 0);
+                }
             }
             mask(b_t1, s);
         }
