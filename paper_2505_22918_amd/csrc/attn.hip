@@ -288,28 +288,35 @@ void attn_fwd(AttnArgs a) {
         return j < 64 ? __builtin_amdgcn_readlane(cols, j) : ((csr_ptr)a.col_idx)[e_beg + j];
     };
     int gen_kb = -1, gen_e = 0;  // complement walk: last block emitted, next kept entry
-    // Key bases of 64 consecutive chunks, one per lane (-1: no key), so a step
-    // reads its chunk's base with one v_readlane instead of a scalar lookup.
-    // Used for the dense walk and for CSR rows of at most 64 entries (whose
-    // column indices all sit in `cols`); the caching walk keeps the scalar path.
-    const bool use_tab = !CACHE && (a.dense || e_end - e_beg <= 64);
-    int tab = -1;
-    auto fill_tab = [&](int i0) {
-        const int i = i0 + lane;
+    // A chunk is addressed by the byte offset of its first key row in the head's
+    // K (or V) buffer, base * 2D, or kOob for a chunk that holds no key.
+    // Except in the caching walk, the offsets of 64 consecutive chunks tb ..
+    // tb+63 sit in one VGPR, lane i holding chunk tb + i (kOob past the row): a
+    // step reads the chunk it loads with one v_readlane and tests no bounds; the
+    // walk refills the table every 64 steps.  The caching walk computes offsets
+    // with scalar code.
+    int tab = kOob, tb = 0;
+    auto fill_tab = [&](int c0) {
+        tb = c0;
+        const int i = c0 + lane;
         const int j = i / (BS / 32), half = i - j * (BS / 32);
-        int kb = a.dense ? j : __builtin_amdgcn_ds_bpermute((j & 63) << 2, cols);
-        const int base = kb * BS + 32 * half;
-        tab = (i < n_chunk && kb >= 0 && kb < a.n_blk && base < T) ? base : -1;
-    };
-    if (use_tab) fill_tab(0);
-    // Key base of chunk i, or -1 for a chunk holding no key.  Called for
-    // i = 0, 1, 2, ... in order, once each (the table refill and the complement
-    // walk rely on it).
-    auto chunk_base = [&](int i) -> int {
-        if (use_tab) {
-            if ((i & 63) == 0 && i > 0) fill_tab(i);
-            return __builtin_amdgcn_readlane(tab, i & 63);
+        int kb = j;
+        if (!a.dense) {
+            if (c0 + 63 < 64 * (BS / 32)) {  // every entry this table needs sits in `cols`
+                kb = __builtin_amdgcn_ds_bpermute((j & 63) << 2, cols);
+            } else {  // a row of more than 64 entries: read them (rare; drains the loads)
+                const int e = i < n_chunk ? e_beg + j : 0;
+                kb = ((const int32_t*)a.col_idx)[e];
+                wait_vm<0>();
+            }
         }
+        const int base = kb * BS + 32 * half;
+        tab = (i < n_chunk && kb >= 0 && kb < a.n_blk && base < T) ? base * (D * 2) : kOob;
+    };
+    if (!CACHE) fill_tab(0);
+    // Offset of chunk i by scalar code.  Called for i = 0, 1, 2, ... in order,
+    // once each (the complement walk relies on it).
+    auto chunk_off = [&](int i) -> int {
         int kb, half;
         if (CACHE && i >= n_in) {
             const int jc = (i - n_in) / (BS / 32);
@@ -336,7 +343,12 @@ void attn_fwd(AttnArgs a) {
             kb = a.dense ? j : kept_at(j);
         }
         const int base = kb * BS + 32 * half;
-        return (kb >= 0 && kb < a.n_blk && base < T) ? base : -1;
+        return (kb >= 0 && kb < a.n_blk && base < T) ? base * (D * 2) : kOob;
+    };
+    // offset of one of the first three chunks
+    auto first_off = [&](int i) -> int {
+        if (CACHE) return i < n_chunk ? chunk_off(i) : kOob;
+        return __builtin_amdgcn_readlane(tab, i);
     };
 
     // LDS map: K(t) in stage t % 3 at [0, 3 TILE), V(t) in stage t % 2 at
@@ -344,15 +356,14 @@ void attn_fwd(AttnArgs a) {
     auto k_off = [&](int st) { return st * TILE; };
     auto v_off = [&](int st) { return (3 + st) * TILE; };
 
-    // DMA of the 32-key chunk starting at key `base` of a head's K or V (buffer
+    // DMA of the 32-key chunk at byte offset `boff` of a head's K or V (buffer
     // resource `rs`: the whole head, T rows) to LDS byte offset `dst`.  Rows past
     // T fall outside the buffer and read as zeros; a chunk that holds no key
-    // (base < 0) is pointed past the buffer, so its loads read zeros and touch no
-    // memory.  Every call issues NDMA loads, so all waits below are constants.
+    // (kOob) lies past the buffer, so its loads read zeros and touch no memory.
+    // Every call issues NDMA loads, so all waits below are constants.
     const i32x4 k_rs = buffer_rsrc(Kh, T * D * 2);
     const i32x4 v_rs = buffer_rsrc(Vh, T * D * 2);
-    auto issue = [&](const i32x4& rs, const int (&off)[NDMA], int base, int dst) {
-        const int boff = base >= 0 ? base * (D * 2) : kOob;
+    auto issue = [&](const i32x4& rs, const int (&off)[NDMA], int boff, int dst) {
         if (NSLOT == 4 * 64) {
             dma16x4(lds0 + dst, off[0] + boff, rs);
         } else {
@@ -399,9 +410,9 @@ void attn_fwd(AttnArgs a) {
             qraw[qt][s] = vload16(ch < DC ? (qt * 32 + l32) * (D * 2) + ch * 16 : kOob, q_rs);
         }
     }
-    const int c0 = n_chunk > 0 ? chunk_base(0) : -1;
-    const int c1 = n_chunk > 1 ? chunk_base(1) : -1;
-    const int c2b = n_chunk > 2 ? chunk_base(2) : -1;
+    const int c0 = first_off(0);
+    const int c1 = first_off(1);
+    const int c2b = first_off(2);
     // issue order Q, K(0), V(0), K(1), K(2); afterwards step t issues K(t+3) at its
     // start and V(t+1) after its P V product, so waiting for V(t-1) at the start of
     // step t leaves exactly three chunk loads (K(t+2), V(t), K(t+3)) in flight
@@ -435,9 +446,9 @@ void attn_fwd(AttnArgs a) {
         for (int dt = 0; dt < DT; ++dt) oacc[qt][dt] = f32x16{};
     }
 
-    // S^T = K Q^T for the K chunk in stage `st`
-    auto qk = [&](int st, f32x16 (&sc)[QT]) {
-        const lds_u8* Ks = lds + k_off(st);
+    // S^T = K Q^T for the K chunk at LDS byte offset `ko`
+    auto qk = [&](int ko, f32x16 (&sc)[QT]) {
+        const lds_u8* Ks = lds + ko;
         bf16x8 kop[DS];
 #pragma unroll
         for (int s = 0; s < DS; ++s) kop[s] = *(const lds_bf16x8*)(Ks + k_rd[s]);
@@ -450,9 +461,12 @@ void attn_fwd(AttnArgs a) {
                 sc[qt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kop[s], qop[qt][s], sc[qt], 0, 0, 0);
         }
     };
-    // keys past T, or a chunk holding no key, score -inf
-    auto mask = [&](int base, f32x16 (&sc)[QT]) {
-        if (base >= 0 && base + 32 <= T) return;
+    // keys past T, or a chunk holding no key, score -inf.  Chunks at offsets up to
+    // full_lim hold 32 keys below T (kOob lies above every such offset).
+    const int full_lim = (T - 32) * (D * 2);
+    auto mask = [&](int boff, f32x16 (&sc)[QT]) {
+        if (boff <= full_lim) return;
+        const int base = boff == kOob ? -1 : boff / (D * 2);
 #pragma unroll
         for (int qt = 0; qt < QT; ++qt) {
 #pragma unroll
@@ -462,21 +476,21 @@ void attn_fwd(AttnArgs a) {
             }
         }
     };
-    // V^T operand of k-step ks of the V chunk in stage `st`: two transpose reads
-    // of 4 key rows each
-    auto v_operand = [&](int st, int dt, int ks) -> bf16x8 {
-        const lds_u8* Vs = lds + v_off(st);
+    // V^T operand of k-step ks of the V chunk at LDS byte offset `vo`: two
+    // transpose reads of 4 key rows each
+    auto v_operand = [&](int vo, int dt, int ks) -> bf16x8 {
+        const lds_u8* Vs = lds + vo;
         const bf16x4 v0 = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(Vs + v_rd[dt] + 16 * ks * ROWB));
         const bf16x4 v1 = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(Vs + v_rd[dt] + (16 * ks + 8) * ROWB));
         return __builtin_shufflevector(v0, v1, 0, 1, 2, 3, 4, 5, 6, 7);
     };
-    // O^T += V^T P^T for the V chunk in stage `st`
-    auto pv = [&](int st, const bf16x8 (&pp)[QT][2]) {
+    // O^T += V^T P^T for the V chunk at LDS byte offset `vo`
+    auto pv = [&](int vo, const bf16x8 (&pp)[QT][2]) {
 #pragma unroll
         for (int dt = 0; dt < DT; ++dt) {
 #pragma unroll
             for (int ks = 0; ks < 2; ++ks) {
-                const bf16x8 vv = v_operand(st, dt, ks);
+                const bf16x8 vv = v_operand(vo, dt, ks);
 #pragma unroll
                 for (int qt = 0; qt < QT; ++qt)
                     oacc[qt][dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vv, pp[qt][ks], oacc[qt][dt], 0, 0, 0);
@@ -585,9 +599,13 @@ void attn_fwd(AttnArgs a) {
 #pragma unroll
         for (int qt = 0; qt < QT; ++qt) m_run[qt] = fmaxf(chunk_max(s[qt]), -1e30f);
     }
-    // rolling window of chunk bases b_t = base(t), b_t1, b_t2; k3 = t % 3
+    // rolling window of chunk offsets b_t = off(t), b_t1, b_t2; LDS byte offsets
+    // of the stages of K(t) (k3) and of V(t) (vo), which moves between the two V
+    // stages by xor with vtog
     int b_t = c0, b_t1 = c1, b_t2 = c2b;
-    int k3 = 0;
+    int k3 = k_off(0);
+    int vo = v_off(0);
+    constexpr int vtog = (3 * TILE) ^ (4 * TILE);
 
     // Step t: issue K(t+3) (HAS_QK) and wait for K(t+1) and V(t-1).  Then
     //   A: P V(t-1) (HAS_PV) on the matrix cores, interleaved with the
@@ -601,12 +619,16 @@ void attn_fwd(AttnArgs a) {
     auto step = [&](int t, auto has_qk, auto has_pv) {
         constexpr bool HAS_QK = decltype(has_qk)::value;
         constexpr bool HAS_PV = decltype(has_pv)::value;
-        const int vst = t & 1;                // stage of V(t)
-        const int kn = k3 == 2 ? 0 : k3 + 1;  // stage of K(t+1)
-        int cn3 = -1;
+        const int vp = vo ^ vtog;                           // stage of V(t-1) and V(t+1)
+        const int kn = k3 == 2 * TILE ? 0 : k3 + TILE;      // stage of K(t+1)
+        int cn3 = kOob;
         if (HAS_QK) {
-            cn3 = t + 3 < n_chunk ? chunk_base(t + 3) : -1;
-            issue(k_rs, kdma, cn3, k_off(k3));  // K(t) was read in step t-1
+            if (!CACHE) {
+                cn3 = __builtin_amdgcn_readlane(tab, t + 3 - tb);  // kOob past the row
+            } else {
+                cn3 = t + 3 < n_chunk ? chunk_off(t + 3) : kOob;
+            }
+            issue(k_rs, kdma, cn3, k3);  // K(t) was read in step t-1
         }
         if (HAS_QK && HAS_PV) {
             wait_vm<3 * NDMA>();  // K(t+2), V(t), K(t+3) may still fly
@@ -620,12 +642,12 @@ void attn_fwd(AttnArgs a) {
 #pragma unroll
             for (int dt = 0; dt < DT; ++dt) {
 #pragma unroll
-                for (int ks = 0; ks < 2; ++ks) vop[dt][ks] = v_operand(vst ^ 1, dt, ks);
+                for (int ks = 0; ks < 2; ++ks) vop[dt][ks] = v_operand(vp, dt, ks);
             }
         }
         bf16x8 kop[DS];
         if (HAS_QK) {
-            const lds_u8* Ks = lds + k_off(kn);
+            const lds_u8* Ks = lds + kn;
 #pragma unroll
             for (int ss = 0; ss < DS; ++ss) kop[ss] = *(const lds_bf16x8*)(Ks + k_rd[ss]);
         }
@@ -666,7 +688,7 @@ void attn_fwd(AttnArgs a) {
         }
         // V(t+1) into the stage P V(t-1) has just read: V gets a step and a half of
         // lead instead of one
-        if (t + 1 < n_chunk) issue(v_rs, vdma, b_t1, v_off(vst ^ 1));
+        if (t + 1 < n_chunk) issue(v_rs, vdma, b_t1, vp);
         if (CACHE && t == n_in && t > 0) flush_kept();  // P V of chunk n_in - 1 is in O
         // Chunk t's bf16 probabilities into pk (P V(t-1) has read it) and the row
         // sums.  With bf16 row sums the S(t+1) product is issued here, between the
@@ -701,7 +723,7 @@ void attn_fwd(AttnArgs a) {
 #pragma unroll
                 for (int ss = 0; ss < DS; ++ss) {
                     const int ch = 2 * ss + hi;
-                    kr[ss] = vload16(b_t >= 0 && ch < DC ? (b_t + l32) * (D * 2) + ch * 16 : kOob, k_rs);
+                    kr[ss] = vload16(b_t != kOob && ch < DC ? b_t + l32 * (D * 2) + ch * 16 : kOob, k_rs);
                 }
                 wait_vm<0>();
 #pragma unroll
@@ -758,6 +780,7 @@ void attn_fwd(AttnArgs a) {
         b_t1 = b_t2;
         b_t2 = cn3;
         k3 = kn;
+        vo = vp;
     };
 
     using yes = std::true_type;
@@ -765,8 +788,16 @@ void attn_fwd(AttnArgs a) {
     if (n_chunk == 1) {
         step(0, no{}, no{});
     } else if (n_chunk > 1) {
+        if (!CACHE) fill_tab(3);  // steps 0 .. 60 load chunks 3 .. 63
         step(0, yes{}, no{});
-        for (int t = 1; t < n_chunk - 1; ++t) step(t, yes{}, yes{});
+        int t = 1;
+        for (;;) {
+            // steps up to tb + 60 find their chunk t + 3 in the table
+            const int t_end = CACHE ? n_chunk - 1 : min(n_chunk - 1, tb + 61);
+            for (; t < t_end; ++t) step(t, yes{}, yes{});
+            if (t >= n_chunk - 1) break;
+            fill_tab(t + 3);
+        }
         step(n_chunk - 1, no{}, yes{});
     }
     if (n_chunk > 0) {
@@ -776,7 +807,7 @@ void attn_fwd(AttnArgs a) {
         } else {
             wait_vm<0>();
         }
-        pv((n_chunk - 1) & 1, pk);  // P V of the last chunk
+        pv(vo ^ vtog, pk);  // P V of the last chunk
     }
     wait_vm<0>();
     if (RESHAPE) {
