@@ -302,7 +302,8 @@ void attn_fwd(AttnArgs a) {
         const int j = i / (BS / 32), half = i - j * (BS / 32);
         int kb = j;
         if (!a.dense) {
-            if (c0 + 63 < 64 * (BS / 32)) {  // every entry this table needs sits in `cols`
+            const int last = (c0 + 63 < n_chunk ? c0 + 63 : n_chunk - 1) / (BS / 32);
+            if (last < 64) {  // every entry this table needs sits in `cols`
                 kb = __builtin_amdgcn_ds_bpermute((j & 63) << 2, cols);
             } else {  // a row of more than 64 entries: read them (rare; drains the loads)
                 const int e = i < n_chunk ? e_beg + j : 0;
