@@ -55,13 +55,37 @@ def executed_flops(wl, n_kept):
     return float(chunks) * 2.0 * wl.block * 32 * (dk + dv) * wl.B * wl.H
 
 
+def _code_only(text):
+    """C++ source with comments removed and whitespace collapsed, so that a
+    digest changes with the code and not with its comments."""
+    out, i, n = [], 0, len(text)
+    while i < n:
+        c = text[i]
+        if c == '"' or c == "'":  # string or char literal, kept whole
+            j = i + 1
+            while j < n and text[j] != c:
+                j += 2 if text[j] == "\\" else 1
+            out.append(text[i:j + 1])
+            i = j + 1
+        elif text.startswith("//", i):
+            j = text.find("\n", i)
+            i = n if j < 0 else j
+        elif text.startswith("/*", i):
+            j = text.find("*/", i + 2)
+            i = n if j < 0 else j + 2
+        else:
+            out.append(c)
+            i += 1
+    return " ".join("".join(out).split())
+
+
 def kernel_source_sha256():
-    """Digest of the attention kernel's sources; a counter summary applies only to
-    the kernel it was taken from."""
+    """Digest of the attention kernel's code (comments and layout ignored); a
+    counter summary applies only to the kernel it was taken from."""
     h = hashlib.sha256()
     for name in ("attn.hip", "kernels.h"):
-        with open(os.path.join(ROOT, "paper_2505_22918_amd", "csrc", name), "rb") as f:
-            h.update(f.read())
+        with open(os.path.join(ROOT, "paper_2505_22918_amd", "csrc", name), encoding="utf-8") as f:
+            h.update(_code_only(f.read()).encode())
     return h.hexdigest()
 
 

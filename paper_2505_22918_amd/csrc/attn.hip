@@ -28,24 +28,24 @@
 // scores are then masked).
 // Rows stay row-major in LDS: K is read as the A operand with 16-byte reads,
 // V^T through ds_read_b64_tr_b16, the CDNA4 LDS transpose read.  16-byte slots
-// of a row are XOR-swizzled by row so both reads are free of bank conflicts
-// (72-wide heads use 144-byte rows, which spread banks as is).
+// of a row are XOR-swizzled by row to spread both reads over the banks (72-wide
+// heads use 144-byte rows, which spread banks as is).
 //
 // Software pipeline.  Step t issues the DMA of K(t+3), runs the P V product of
 // chunk t-1 on the matrix cores under the exponentials of chunk t's softmax,
 // issues the DMA of V(t+1) into the stage V(t-1) has just left, packs chunk t's
-// probabilities to bf16 in the registers P V(t-1)
-// has just read, and computes S(t+1) = K Q^T into the registers softmax(t) has
-// just read (no register copies between steps).  The last step has no S
-// product; the residual loads are issued there.
+// probabilities to bf16 in the registers P V(t-1) has just read, and computes
+// S(t+1) = K Q^T into the registers softmax(t) has just read (no register
+// copies between steps).  The last step has no S product; the residual loads
+// are issued there.
 //
 // Softmax.  The running max starts at the first chunk's max and moves only
 // when a chunk's probabilities against it reach 2^64 (far below fp32 and bf16
 // overflow); that rare case rescales O and l and recomputes the chunk.
-// Without requested statistics no per-chunk max is taken:
-// the overflow test reads the chunk's row sum.  With statistics the exact max
-// is tracked and l is moved to it at the end, so the emitted pair is exactly
-// max and exp-sum.
+// Without requested statistics no per-chunk max is taken: the overflow test
+// reads the chunk's row sum, which then adds the bf16 probabilities P V uses.
+// With statistics the exact max is tracked and l, summed in fp32, is moved to
+// it at the end, so the emitted pair is exactly max and exp-sum.
 
 #include <hip/hip_runtime.h>
 #include <stdint.h>
