@@ -172,6 +172,9 @@ def main():
     ap.add_argument("--cpu-budget", type=float, default=12.0)
     ap.add_argument("--cold-iters", type=int, default=5,
                     help="calls timed one by one after a 512 MiB write that flushes L2 and MALL")
+    ap.add_argument("--zero-queries", action="store_true",
+                    help="diagnostic: feed zero queries (every score 0) to the timed calls; the same "
+                         "kernel runs with less switching, which shows how the clock depends on the data")
     ap.add_argument("--copy-mb", type=int, default=0,
                     help="also run K plain device copies of this many MiB (HBM counter calibration)")
     args = ap.parse_args()
@@ -210,6 +213,9 @@ def main():
 
     q1, k1, v1 = (to_dev(x) for x in s1)
     q2, k2, v2 = (to_dev(x) for x in s2)
+    if args.zero_queries:
+        q2.zero_()
+        log("diagnostic run: zero queries in the timed calls")
     stream = torch.cuda.current_stream()
 
     # caching step on step-1 inputs
@@ -361,7 +367,7 @@ def main():
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "bf16",
-        "data": "synthetic",
+        "data": "synthetic, zero queries (diagnostic)" if args.zero_queries else "synthetic",
         "config": {
             "workload": wl.name,
             "B": wl.B, "H": wl.H, "T": wl.T, "D": wl.D, "block": wl.block,
