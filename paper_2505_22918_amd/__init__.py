@@ -19,9 +19,11 @@ import ctypes
 from dataclasses import dataclass
 
 from . import _lib
+from ._lib import RettentionError
 from .synth import PAT_EXPLICIT, PAT_LOCAL2D, PAT_VIDEO3D
 
 __all__ = [
+    "RettentionError",
     "BlockMask",
     "index_size",
     "build_index",
