@@ -93,6 +93,20 @@ def block_index_local2d(T, bs, grid_h, grid_w, keep):
     return _to_csr(rows)
 
 
+def local2d_rows(T, bs, grid_h, grid_w, keep, qblocks):
+    """The kept key blocks of the listed query blocks only, by the same centroids
+    and ranking as block_index_local2d (for masks too large to rank every row)."""
+    if grid_h * grid_w != T:
+        raise ValueError("grid_h * grid_w must equal T")
+    nb = n_blocks(T, bs)
+    cent = [
+        _centroid([(t // grid_w, t % grid_w) for t in _block_tokens(b, bs, T)])
+        for b in range(nb)
+    ]
+    k = min(keep, nb)
+    return [_rank_keep(int(qb), range(nb), cent, k) for qb in qblocks]
+
+
 def block_index_video3d(T, bs, n_text, frames, grid_h, grid_w, keep):
     """Text prefix + spatio-temporal local window on frames x grid_h x grid_w."""
     if n_text + frames * grid_h * grid_w != T:

@@ -64,3 +64,25 @@ def test_explicit_dense_and_random(gpu):
     for nb, extra, seed in [(7, 6, 0), (33, 3, 1), (130, 2, 2)]:
         hm = synth.explicit_block_mask(nb, seed=seed, extra=extra)
         _check(nb * 32 - 5, 32, synth.PAT_EXPLICIT, ob.block_index_explicit(hm), host_mask=hm)
+
+
+def test_largest_index_build(gpu):
+    """The builder at its limit of 4096 blocks per side: a 512 x 512 image latent
+    in 64-token blocks keeping 1/32 of them.  Sampled rows bit-exact against the
+    oracle, every row checked for shape (ascending, keep entries, diagonal)."""
+    gh = gw = 512
+    T, bs = gh * gw, 64
+    nb = T // bs
+    keep = nb // 32
+    print(f"[index] largest: T={T} nb={nb} keep={keep}", flush=True)
+    m = rt.build_index(T, bs, synth.PAT_LOCAL2D, grid_h=gh, grid_w=gw, keep=keep)
+    rp, ci = _gpu_csr(m)
+    assert m.n_qblk == nb and m.nnz == nb * keep
+    np.testing.assert_array_equal(rp, np.arange(nb + 1) * keep)
+    rows = ci.reshape(nb, keep)
+    assert np.all(np.diff(rows, axis=1) > 0)
+    assert np.all((rows >= 0) & (rows < nb))
+    assert np.all((rows == np.arange(nb)[:, None]).any(axis=1))
+    sample = [0, 1, 7, 8, 511, 1000, 2047, 2048, 3333, 4088, 4095]
+    for qb, r in zip(sample, ob.local2d_rows(T, bs, gh, gw, keep, sample)):
+        np.testing.assert_array_equal(rows[qb], r)

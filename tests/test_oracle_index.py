@@ -142,3 +142,11 @@ def test_explicit_mask_roundtrip():
     rp, ci = ob.block_index_explicit(m)
     np.testing.assert_array_equal(ob.dense_mask(rp, ci, 9), m)
     assert np.all(np.diag(m) == 1) and np.all(m.sum(axis=1) == 3)
+
+
+def test_local2d_rows_agree_with_the_full_build():
+    T, bs, gh, gw, keep = 25 * 40, 64, 25, 40, 3
+    rp, ci = ob.block_index_local2d(T, bs, gh, gw, keep)
+    rows = ob.local2d_rows(T, bs, gh, gw, keep, range(len(rp) - 1))
+    for qb, r in enumerate(rows):
+        assert r == ci[rp[qb]:rp[qb + 1]].tolist()
