@@ -330,6 +330,16 @@ def main():
                       f"attention + reshape; {t_cpu:.1f} s",
             "ms_per_call_extrapolated": t_cpu / frac * 1e3,
         }
+        # the oracle's dense attention (Eq.1 / Eq.4) on one (batch, head) pair,
+        # scaled to the whole call
+        from oracle import attention as oa
+
+        f64 = lambda b: synth.bf16_bits_to_f32(b).astype(np.float64)
+        t0 = time.perf_counter()
+        oa.full_attention(f64(s2[0][:1, :1]), f64(s2[1][:1, :1]), f64(s2[2][:1, :1]))
+        t_dense_cpu = time.perf_counter() - t0
+        cpu["dense_sample"] = f"1 of {wl.B * wl.H} (batch, head) pairs, fp64 NumPy dense attention; {t_dense_cpu:.1f} s"
+        cpu["dense_ms_per_call_extrapolated"] = t_dense_cpu * wl.B * wl.H * 1e3
         log(f"cpu oracle: {cpu}")
 
     bound = "hbm" if ai < ridge else "mfma"
@@ -343,7 +353,7 @@ def main():
         "frac": (gbs / PEAK_HBM_GBS) if bound == "hbm" else (tflops / PEAK_BF16_TFLOPS),
         "traffic": traffic,
         "traffic_over_algorithmic": (traffic / nbytes) if traffic else None,
-        "kernel": f"attn_fwd<{wl.D},{wl.block},reshape=true,stats=false>",
+        "kernel": f"attn_fwd<{wl.D},{wl.block},reshape=true,stats=false,cache=false>",
         "algorithmic_bytes": nbytes,
         "algorithmic_flops": flops,
         "executed_mfma_flops": exec_flops,
