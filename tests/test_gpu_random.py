@@ -1,0 +1,109 @@
+"""Seeded random configurations against the fp64 oracle, every call mode.
+
+Each case draws a shape (batch, heads, a token count with a ragged tail, head
+width 64 or 72, block 32 or 64), a mask layout (one shared mask, one per head,
+one per (batch, head)) and random explicit masks with rows of one to every key
+block, then checks sparse attention with and without statistics, the fused
+reshape (Eq.9 with a ramp, Eq.10), dense attention with statistics (Eq.1,
+Eq.4), the one-pass caching step (Eq.8, Eq.10) and post-softmax masking (Eq.7)
+element by element.
+"""
+
+import numpy as np
+import pytest
+
+import paper_2505_22918_amd as rt
+from oracle import attention as oa
+from oracle import block_index as ob
+from paper_2505_22918_amd import synth
+
+from parity import assert_bf16_close, assert_stat_close, to_dev, to_np
+
+pytestmark = pytest.mark.gpu
+
+N_CASES = 24
+
+
+def _case(i):
+    rng = np.random.default_rng(1000 + i)
+    B = int(rng.integers(1, 3))
+    H = int(rng.integers(1, 4))
+    D = int(rng.choice([64, 72]))
+    block = int(rng.choice([32, 64]))
+    T = int(rng.integers(1, 12)) * block - int(rng.integers(0, block))
+    T = max(T, 1)
+    layout = str(rng.choice(["shared", "head", "batch_head"]))
+    return dict(B=B, H=H, T=T, D=D, block=block, layout=layout, seed=1000 + i)
+
+
+def _random_masks(n_masks, nb, rng):
+    masks = []
+    for _ in range(n_masks):
+        m = np.zeros((nb, nb), dtype=np.uint8)
+        for r in range(nb):
+            m[r, r] = 1  # every row keeps a block (Eq.5 needs a non-empty set)
+            k = int(rng.integers(0, nb))  # 0 .. nb-1 more blocks: up to every block
+            if k:
+                m[r, rng.choice(nb, size=k, replace=False)] = 1
+        masks.append(m)
+    return np.stack(masks)
+
+
+@pytest.mark.parametrize("i", range(N_CASES))
+def test_random_configuration(gpu, i):
+    import torch
+
+    c = _case(i)
+    B, H, T, D, block = c["B"], c["H"], c["T"], c["D"], c["block"]
+    nb = ob.n_blocks(T, block)
+    n_masks = {"shared": 1, "head": H, "batch_head": B * H}[c["layout"]]
+    print(f"[random] case {i}: {c}", flush=True)
+    rng = np.random.default_rng(c["seed"])
+    hm = _random_masks(n_masks, nb, rng)
+    mask = rt.build_index(T, block, synth.PAT_EXPLICIT, host_mask=hm if n_masks > 1 else hm[0])
+    csrs = [ob.block_index_explicit(hm[m]) for m in range(n_masks)]
+
+    shape = (B, H, T, D)
+    s = [synth.f32_to_bf16_bits(rng.standard_normal(shape, dtype=np.float32) * np.float32(sc))
+         for sc in (1.5, 1.0, 1.0)]
+    q, k, v = (to_dev(x) for x in s)
+    rho = torch.from_numpy(rng.uniform(0.0, 1.0, size=(B, H, T)).astype(np.float32)).cuda()
+    resid = torch.from_numpy((0.05 * rng.standard_normal(shape)).astype(np.float32)).cuda().to(torch.bfloat16)
+    delta = float(rng.choice([0.0, 0.04, 0.5]))
+
+    o_st, m_st, l_st = rt.attn_sparse(q, k, v, mask, stats=True)
+    o_ns = rt.attn_sparse(q, k, v, mask, stats=False)
+    o_fu = rt.attn_sparse_reshape(q, k, v, mask, rho, resid, rho_delta=delta)
+    of, mf, lf = rt.attn_full(q, k, v, block=block)
+    oc, rhoc, rc, mc, lc = rt.attn_cache(q, k, v, mask)
+    op = rt.attn_postmask(q, k, v, mask)
+    torch.cuda.synchronize()
+
+    Q, K, V = (synth.bf16_bits_to_f32(x).astype(np.float64) for x in s)
+    Of, Mf, Lf = oa.full_attention(Q, K, V)
+    assert_bf16_close(to_np(of), Of, f"case {i} O_full")
+    assert_stat_close(to_np(mf), Mf, f"case {i} m_full", floor=1.0)
+    assert_stat_close(to_np(lf), Lf, f"case {i} l_full")
+    rho_h, resid_h = to_np(rho), to_np(resid)
+    got = {n: to_np(t) for n, t in dict(o_st=o_st, m_st=m_st, l_st=l_st, o_ns=o_ns, o_fu=o_fu, oc=oc, rhoc=rhoc,
+                                         rc=rc, mc=mc, lc=lc, op=op).items()}
+    for b in range(B):
+        for h in range(H):
+            mid = 0 if n_masks == 1 else (h if n_masks == H else b * H + h)
+            rp, ci = csrs[mid]
+            sl = (slice(b, b + 1), slice(h, h + 1))
+            Os, Ms, Ls = oa.sparse_attention(Q[sl], K[sl], V[sl], rp, ci, block)
+            Rho = oa.rho(Ms, Ls, Mf[sl], Lf[sl])
+            R = oa.residual(Of[sl], Os, Rho)
+            tag = f"case {i} (b={b}, h={h})"
+            assert_bf16_close(got["o_st"][sl], Os, f"{tag} O_s")
+            assert_stat_close(got["m_st"][sl], Ms, f"{tag} m_s", floor=1.0)
+            assert_stat_close(got["l_st"][sl], Ls, f"{tag} l_s")
+            assert_bf16_close(got["o_ns"][sl], Os, f"{tag} O_s without statistics")
+            assert_bf16_close(got["o_fu"][sl], oa.reshape(Os, rho_h[sl], resid_h[sl], delta), f"{tag} fused")
+            assert_bf16_close(got["oc"][sl], Of[sl], f"{tag} caching O_full")
+            assert_stat_close(got["rhoc"][sl], Rho, f"{tag} caching rho", floor=1e-6)
+            assert_bf16_close(got["rc"][sl], R, f"{tag} caching R")
+            assert_stat_close(got["mc"][sl], Mf[sl], f"{tag} caching m", floor=1.0)
+            assert_stat_close(got["lc"][sl], Lf[sl], f"{tag} caching l")
+            assert_bf16_close(got["op"][sl], Rho[..., None] * Os, f"{tag} (A o M) V")
