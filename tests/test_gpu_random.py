@@ -107,3 +107,47 @@ def test_random_configuration(gpu, i):
             assert_stat_close(got["mc"][sl], Mf[sl], f"{tag} caching m", floor=1.0)
             assert_stat_close(got["lc"][sl], Lf[sl], f"{tag} caching l")
             assert_bf16_close(got["op"][sl], Rho[..., None] * Os, f"{tag} (A o M) V")
+
+
+# Long rows: 40 to 150 kept blocks, so walks cross the 64-chunk table refill and,
+# past 64 entries, the refill that reads column indices from memory.
+LONG = [(1, 1, 150 * 32 - 7, 64, 32, 70, 150), (1, 2, 90 * 64 - 30, 64, 64, 40, 80),
+        (2, 1, 130 * 32, 72, 32, 100, 130), (1, 1, 70 * 64 - 1, 72, 64, 60, 70)]
+
+
+@pytest.mark.parametrize("case", LONG, ids=[f"long{i}" for i in range(len(LONG))])
+def test_long_rows(gpu, case):
+    import torch
+
+    B, H, T, D, block, kmin, kmax = case
+    nb = ob.n_blocks(T, block)
+    print(f"[random] long rows B={B} H={H} T={T} D={D} block={block} keep {kmin}..{kmax}", flush=True)
+    rng = np.random.default_rng(T)
+    hm = np.zeros((nb, nb), dtype=np.uint8)
+    for r in range(nb):
+        hm[r, r] = 1
+        k = int(rng.integers(kmin, min(kmax, nb) + 1)) - 1
+        others = np.array([c for c in range(nb) if c != r])
+        hm[r, rng.choice(others, size=min(k, len(others)), replace=False)] = 1
+    mask = rt.build_index(T, block, synth.PAT_EXPLICIT, host_mask=hm)
+    rp, ci = ob.block_index_explicit(hm)
+    shape = (B, H, T, D)
+    s = [synth.f32_to_bf16_bits(rng.standard_normal(shape, dtype=np.float32)) for _ in range(3)]
+    q, k, v = (to_dev(x) for x in s)
+    rho = torch.full((B, H, T), 0.3, device="cuda")
+    resid = torch.zeros(shape, device="cuda", dtype=torch.bfloat16)
+    o_st, m_st, l_st = rt.attn_sparse(q, k, v, mask, stats=True)
+    o_fu = rt.attn_sparse_reshape(q, k, v, mask, rho, resid, rho_delta=0.0)
+    oc, rhoc, rc, mc, lc = rt.attn_cache(q, k, v, mask)
+    torch.cuda.synchronize()
+    Q, K, V = (synth.bf16_bits_to_f32(x).astype(np.float64) for x in s)
+    Os, Ms, Ls = oa.sparse_attention(Q, K, V, rp, ci, block)
+    Of, Mf, Lf = oa.full_attention(Q, K, V)
+    Rho = oa.rho(Ms, Ls, Mf, Lf)
+    assert_bf16_close(to_np(o_st), Os, "long rows O_s")
+    assert_stat_close(to_np(m_st), Ms, "long rows m_s", floor=1.0)
+    assert_stat_close(to_np(l_st), Ls, "long rows l_s")
+    assert_bf16_close(to_np(o_fu), oa.reshape(Os, to_np(rho), to_np(resid), 0.0), "long rows fused")
+    assert_bf16_close(to_np(oc), Of, "long rows caching O_full")
+    assert_stat_close(to_np(rhoc), Rho, "long rows caching rho", floor=1e-6)
+    assert_bf16_close(to_np(rc), oa.residual(Of, Os, Rho), "long rows caching R")
