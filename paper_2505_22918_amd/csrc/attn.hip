@@ -17,7 +17,7 @@
 // exactly the 8+8 key values the B operand of the P V product needs, so P
 // never leaves registers.  The rows of the V^T operand are permuted so that
 // each lane's 16 accumulator values of O^T are 16 consecutive head dims of
-// its query: the residual tile arrives and the output leaves as 16-byte
+// its query: the residual rows are read and the output leaves as 16-byte
 // vector loads and stores straight from registers.
 //
 // Memory.  Q arrives by buffer loads straight into its B-operand registers.
@@ -36,8 +36,10 @@
 // issues the DMA of V(t+1) into the stage V(t-1) has just left, packs chunk t's
 // probabilities to bf16 in the registers P V(t-1) has just read, and computes
 // S(t+1) = K Q^T into the registers softmax(t) has just read (no register
-// copies between steps).  The last step has no S product; the residual loads
-// are issued there.
+// copies between steps).  The last step has no S product.  In the fused
+// reshape the K loads of the two chunks past the row, which would only read
+// zeros, bring the block's residual rows into their K stages instead, two to
+// three steps before the epilogue reads them.
 //
 // Softmax.  The running max starts at the first chunk's max and moves only
 // when a chunk's probabilities against it reach 2^64 (far below fp32 and bf16
@@ -67,6 +69,7 @@ typedef const __attribute__((address_space(4))) int32_t* csr_ptr;
 typedef __attribute__((address_space(3))) unsigned char lds_u8;
 typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
 typedef __attribute__((address_space(3))) bf16x8 lds_bf16x8;
+typedef __attribute__((address_space(3))) u32x4 lds_u32x4;
 
 constexpr float kJump = 18446744073709551616.0f;  // 2^64: stale-max limit on a probability
 constexpr int kOob = 0x40000000;                   // buffer offset past every record: reads zero
@@ -189,7 +192,6 @@ void attn_fwd(AttnArgs a) {
     constexpr int TILE = 32 * ROWB;          // LDS bytes per K or V chunk
     constexpr int NSLOT = 32 * G::SLOTS;     // 16-byte slots per chunk and tensor
     constexpr int NDMA = (NSLOT + 63) / 64;  // DMA instructions per chunk and tensor
-    constexpr int NR = QT * DT * 2;          // residual loads per lane
     // three K stages and two V stages (+ slack for the padded V^T reads of a 72-wide
     // head): 20 KB per wave at D = 64, so 8 waves fill a CU's 160 KB
     constexpr int SMEM = 5 * TILE + (D == 64 ? 0 : 256);
@@ -374,23 +376,21 @@ void attn_fwd(AttnArgs a) {
             }
         }
     };
-    // residual tile in the O^T accumulator layout: lane (hi, l32) of tile (qt, dt)
-    // takes row 32qt + l32, head dims 32dt + 16hi .. +15 as two 16-byte loads
-    u32x4 rraw[QT][DT][2];
-    auto issue_resid = [&]() {
-        const i32x4 rs = buffer_rsrc(a.resid + head_off + (size_t)row0 * D, nrow * D * 2);
-#pragma unroll
-        for (int qt = 0; qt < QT; ++qt) {
-#pragma unroll
-            for (int dt = 0; dt < DT; ++dt) {
-#pragma unroll
-                for (int u = 0; u < 2; ++u) {
-                    const int ch = 4 * dt + 2 * hi + u;
-                    const int off = ch < DC ? (qt * 32 + l32) * (D * 2) + ch * 16 : kOob;
-                    rraw[qt][dt][u] = vload16(off, rs);
-                }
+    // K load of chunk c into LDS byte offset dst.  In the fused reshape the loads
+    // of chunks n_chunk .. n_chunk + QT - 1, which lie past the row and would only
+    // fill their stages with zeros, instead bring the block's residual rows
+    // 32j .. 32j + 31 (j = c - n_chunk) in the K layout: R lands two to three steps
+    // before the epilogue reads it, with the same number of loads per step.
+    const i32x4 r_rs = RESHAPE ? buffer_rsrc(a.resid + head_off + (size_t)row0 * D, nrow * D * 2) : k_rs;
+    auto issue_k = [&](int c, int boff, int dst) {
+        if (RESHAPE) {
+            const int rj = c - n_chunk;
+            if (rj >= 0 && rj < QT) {
+                issue(r_rs, kdma, rj * 32 * (D * 2), dst);
+                return;
             }
         }
+        issue(k_rs, kdma, boff, dst);
     };
 
     // ---- prologue ---------------------------------------------------------------------
@@ -417,12 +417,11 @@ void attn_fwd(AttnArgs a) {
     // issue order Q, K(0), V(0), K(1), K(2); afterwards step t issues K(t+3) at its
     // start and V(t+1) after its P V product, so waiting for V(t-1) at the start of
     // step t leaves exactly three chunk loads (K(t+2), V(t), K(t+3)) in flight
-    issue(k_rs, kdma, c0, k_off(0));
+    issue_k(0, c0, k_off(0));
     issue(v_rs, vdma, c0, v_off(0));
-    issue(k_rs, kdma, c1, k_off(1));
-    issue(k_rs, kdma, c2b, k_off(2));
+    issue_k(1, c1, k_off(1));
+    issue_k(2, c2b, k_off(2));
     wait_vm<3 * NDMA>();  // Q and K(0) have landed
-    if (RESHAPE && n_chunk == 0) issue_resid();
     bf16x8 qop[QT][DS];
 #pragma unroll
     for (int qt = 0; qt < QT; ++qt) {
@@ -616,7 +615,7 @@ void attn_fwd(AttnArgs a) {
     //      max, chunk t is recomputed; P V(t-1) is in O by then);
     //   B: chunk t's bf16 probabilities into pk (P V(t-1) has read it), then
     //      S(t+1) = K Q^T (HAS_QK) into s (softmax(t) has read it).
-    // The step without S product is the last one; it issues the residual loads.
+    // The step without S product is the last one.
     auto step = [&](int t, auto has_qk, auto has_pv) {
         constexpr bool HAS_QK = decltype(has_qk)::value;
         constexpr bool HAS_PV = decltype(has_pv)::value;
@@ -629,14 +628,13 @@ void attn_fwd(AttnArgs a) {
             } else {
                 cn3 = t + 3 < n_chunk ? chunk_off(t + 3) : kOob;
             }
-            issue(k_rs, kdma, cn3, k3);  // K(t) was read in step t-1
+            issue_k(t + 3, cn3, k3);  // K(t) was read in step t-1
         }
         if (HAS_QK && HAS_PV) {
             wait_vm<3 * NDMA>();  // K(t+2), V(t), K(t+3) may still fly
         } else if (HAS_QK || HAS_PV) {
             wait_vm<2 * NDMA>();  // step 0: K(2), K(3); last step: K(t+2), V(t)
         }
-        if (!HAS_QK && RESHAPE) issue_resid();
 
         bf16x8 vop[DT][2];
         if (HAS_PV) {
@@ -801,26 +799,9 @@ void attn_fwd(AttnArgs a) {
         }
         step(n_chunk - 1, no{}, yes{});
     }
-    if (n_chunk > 0) {
-        // V(n-1) has landed once only the residual loads may be outstanding
-        if (RESHAPE) {
-            wait_vm<NR>();
-        } else {
-            wait_vm<0>();
-        }
-        pv(vo ^ vtog, pk);  // P V of the last chunk
-    }
-    wait_vm<0>();
-    if (RESHAPE) {
-#pragma unroll
-        for (int qt = 0; qt < QT; ++qt) {
-#pragma unroll
-            for (int dt = 0; dt < DT; ++dt) {
-                settle(rraw[qt][dt][0]);
-                settle(rraw[qt][dt][1]);
-            }
-        }
-    }
+    wait_vm<0>();  // V(n-1) and, in the fused reshape, the residual rows
+    asm volatile("" ::: "memory");  // no LDS read moves above the wait
+    if (n_chunk > 0) pv(vo ^ vtog, pk);  // P V of the last chunk
 
     if (CACHE) {
         // ---- caching-step epilogue (App. A.3): with l_in, l_out and acc_out
@@ -930,7 +911,10 @@ void attn_fwd(AttnArgs a) {
 #pragma unroll
                     for (int e = 0; e < 8; ++e) y[e] = oacc[qt][dt][8 * u + e] * factor;
                     if (RESHAPE) {
-                        const u32x4 r4 = rraw[qt][dt][u];
+                        // residual row rl, head dims 8ch .. 8ch+7, from the K stage
+                        // of chunk n_chunk + qt
+                        const lds_u8* Rs = lds + k_off((n_chunk + qt) % 3);
+                        const u32x4 r4 = *(const lds_u32x4*)(Rs + l32 * ROWB + ((ch ^ kswz<D>(l32)) * 16));
 #pragma unroll
                         for (int w = 0; w < 4; ++w) {
                             y[2 * w] += lo_f(r4[w]);
