@@ -24,7 +24,7 @@ reshape           Eq.9 + ramp (Sec.4.2) + residual: min(1, rho + delta) O_s + R
 brute_force       Eq.2-5, 7, 8, 10 and the App. A.3 decomposition written as
                   literal T x T matrices (tiny inputs only)
 
-Readings of the paper taken here (each is listed with its reason in the design notes):
+Readings of the paper taken here, where its text leaves the choice open:
   * rho is one value per (batch, head, query row)  (Eq.8 indexes k, i).
   * the ramp rho_t = rho_{t-1} + lambda (Sec.4.2) is applied as
     rho_c + lambda * (t - c) from the caching step c and clamped to at most 1,
