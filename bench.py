@@ -181,7 +181,7 @@ def main():
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py runs on one GPU only: the attention path is sharded by heads with no "
-              "collective, and this build measures the one-GPU share (use --gpus 1).", file=sys.stderr)
+              "collective, and the benchmark measures the one-GPU share (use --gpus 1).", file=sys.stderr)
         sys.exit(2)
 
     import torch

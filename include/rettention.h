@@ -44,7 +44,7 @@ extern "C" {
 typedef enum {
     RT_OK = 0,
     RT_EINVAL = 1,       /* a null pointer, a negative or inconsistent size  */
-    RT_EUNSUPPORTED = 2, /* a head width or block size this build lacks      */
+    RT_EUNSUPPORTED = 2, /* a head width or block size the library lacks    */
     RT_ECAPACITY = 3,    /* an output buffer smaller than the result needs   */
     RT_EHIP = 4          /* the HIP runtime refused a launch                 */
 } rt_status;
