@@ -10,6 +10,8 @@ library (the binding only marshals pointers and sizes).
   cache_build           rho and residual at a caching step (Eq.8, Eq.10)
   attn_sparse_reshape   fused sparse attention + reshape + residual (Eq.5, 9, 10)
   reshape_apply         the reshape on a precomputed sparse output (Eq.9, 10)
+  attn_cache            one-pass caching step: O_full, rho and R (App. A.3, Eq.8, 10)
+  attn_postmask         post-softmax masking (A o M) V (Eq.7)
   StatCache             per-layer cache of rho and R with the step schedule of Sec.5
 """
 
