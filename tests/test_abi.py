@@ -26,6 +26,16 @@ def test_exports_every_header_symbol(lib):
         assert hasattr(lib, n), n
 
 
+def test_missing_library_fails_loudly(tmp_path, monkeypatch):
+    # no fallback: without the built library every call raises instead of computing elsewhere
+    monkeypatch.setattr(_lib, "_lib", None)
+    with pytest.raises(RuntimeError, match="no fallback"):
+        _lib.load(str(tmp_path / "librettention.so"))
+    monkeypatch.setattr(_lib.load, "__defaults__", (str(tmp_path / "librettention.so"),))
+    with pytest.raises(RuntimeError, match="not found"):
+        rt.index_size(256, 64, synth.PAT_LOCAL2D, grid_h=16, grid_w=16, keep=1)
+
+
 def test_status_strings(lib):
     for s in range(5):
         assert lib.rt_status_str(s)
