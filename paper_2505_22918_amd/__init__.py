@@ -43,29 +43,40 @@ __all__ = [
 ]
 
 
-def _torch():
-    import torch
+_TORCH = None
 
-    return torch
+
+def _torch():
+    global _TORCH
+    if _TORCH is None:
+        import torch
+
+        _TORCH = torch
+    return _TORCH
 
 
 def _stream(t):
+    """Raw handle of torch's current stream on t's device (the calls launch there)."""
     torch = _torch()
-    return ctypes.c_void_p(torch.cuda.current_stream(t.device).cuda_stream)
+    raw = getattr(torch._C, "_cuda_getCurrentRawStream", None)
+    if raw is not None:
+        return raw(t.get_device())
+    return torch.cuda.current_stream(t.device).cuda_stream
 
 
 def _ptr(t):
-    return ctypes.c_void_p(t.data_ptr()) if t is not None else ctypes.c_void_p(0)
+    """Device address of t, or NULL for None (ctypes takes ints for void*)."""
+    return t.data_ptr() if t is not None else None
 
 
 def _check_qkv(q, k, v):
     torch = _torch()
     for name, t in (("q", q), ("k", k), ("v", v)):
-        if not isinstance(t, torch.Tensor) or t.device.type != "cuda":
+        if not isinstance(t, torch.Tensor) or not t.is_cuda:
             raise ValueError(f"{name} must be a CUDA tensor")
-        if t.dtype != torch.bfloat16 or t.dim() != 4 or not t.is_contiguous():
+        if t.dtype is not torch.bfloat16 or t.dim() != 4 or not t.is_contiguous():
             raise ValueError(f"{name} must be a contiguous bf16 [B,H,T,D] tensor")
-        if t.shape != q.shape or t.device != q.device:
+        if t is not q and (t.shape != q.shape or t.get_device() != q.get_device()):
             raise ValueError("q, k, v must share shape and device")
     B, H, T, D = q.shape
     return _lib.RtDims(B, H, T, D)
@@ -73,14 +84,14 @@ def _check_qkv(q, k, v):
 
 def _stat(t, shape, name):
     torch = _torch()
-    if t.dtype != torch.float32 or tuple(t.shape) != tuple(shape) or not t.is_contiguous():
+    if t.dtype is not torch.float32 or t.shape != shape or not t.is_contiguous():
         raise ValueError(f"{name} must be a contiguous fp32 tensor of shape {tuple(shape)}")
     return t
 
 
 def _bf16(t, shape, name):
     torch = _torch()
-    if t.dtype != torch.bfloat16 or tuple(t.shape) != tuple(shape) or not t.is_contiguous():
+    if t.dtype is not torch.bfloat16 or t.shape != shape or not t.is_contiguous():
         raise ValueError(f"{name} must be a contiguous bf16 tensor of shape {tuple(shape)}")
     return t
 
@@ -99,8 +110,13 @@ class BlockMask:
     n_masks: int = 1
 
     def c_struct(self):
-        return _lib.RtBsr(self.row_ptr.data_ptr(), self.col_idx.data_ptr(), self.block, self.n_qblk,
-                          self.nnz, self.n_masks)
+        """The rt_bsr view of this mask (built once: a mask is not modified after it is made)."""
+        c = self.__dict__.get("_c")
+        if c is None:
+            c = _lib.RtBsr(self.row_ptr.data_ptr(), self.col_idx.data_ptr(), self.block, self.n_qblk, self.nnz,
+                           self.n_masks)
+            self.__dict__["_c"] = c
+        return c
 
     @classmethod
     def from_csr(cls, row_ptr, col_idx, block, device="cuda", n_masks=1):
