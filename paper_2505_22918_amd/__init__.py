@@ -96,7 +96,7 @@ def _bf16(t, shape, name):
     return t
 
 
-@dataclass
+@dataclass(frozen=True)
 class BlockMask:
     """Block CSR on the device: row_ptr [n_masks][n_qblk+1] (absolute offsets),
     col_idx [nnz] (int32).  n_masks is 1 (shared by every head), H (per head) or
