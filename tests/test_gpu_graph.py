@@ -1,4 +1,5 @@
-"""The library's calls captured in a HIP graph (through torch.cuda.CUDAGraph).
+"""The library's calls captured in a HIP graph (through torch.cuda.CUDAGraph), and
+on a non-default stream.
 
 Every call launches its kernels on the caller's stream and allocates nothing, so
 a decoding or denoising loop can capture it.  Each replay here is checked
@@ -93,3 +94,25 @@ def test_caching_step_and_fused_call_replay_together(gpu):
         assert torch.equal(cache["rho"], e_rho), f"replay {i}: rho"
         assert torch.equal(cache["resid"], e_resid), f"replay {i}: R"
         assert torch.equal(out, e_out), f"replay {i}: fused output"
+
+
+def test_calls_follow_the_current_stream(gpu):
+    import torch
+
+    print("[stream] fused call on a side stream", flush=True)
+    mask, q, k, v = _setup(seed=5)
+    o_full, rho, resid, _, _ = rt.attn_cache(q, k, v, mask)
+    ref = rt.attn_sparse_reshape(q, k, v, mask, rho, resid, rho_delta=0.0)
+    torch.cuda.synchronize()
+    side = torch.cuda.Stream()
+    out = torch.empty_like(q)
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        # producer and consumer on the side stream: the call must launch there,
+        # after the write of q and before the copy of its result
+        q2 = q.clone()
+        rt.attn_sparse_reshape(q2, k, v, mask, rho, resid, rho_delta=0.0, out=out)
+        res = out.clone()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    assert torch.equal(res, ref)
