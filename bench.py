@@ -132,7 +132,10 @@ def time_calls(fn, iters, stream):
 
 
 def cpu_baseline(wl, s2, rp, ci, rho, resid, budget_s=12.0):
-    """The oracle's sparse+reshape step on whole heads until ~budget_s of work."""
+    """The oracle's sparse+reshape step on whole (batch, head) pairs until about
+    budget_s of work; a workload that finishes sooner is run again whole, so
+    the rate rests on at least budget_s of timing.  Returns the time, the pairs
+    evaluated (counting repeats), the pairs in one call and the BLAS threads."""
     from oracle import attention as oa
     from paper_2505_22918_amd import synth
 
@@ -146,19 +149,19 @@ def cpu_baseline(wl, s2, rp, ci, rho, resid, budget_s=12.0):
     heads = [(b, h) for b in range(wl.B) for h in range(wl.H)]
     done = 0
     t_total = 0.0
-    for (b, h) in heads:
-        q = f(s2[0][b:b + 1, h:h + 1])
-        k = f(s2[1][b:b + 1, h:h + 1])
-        v = f(s2[2][b:b + 1, h:h + 1])
-        t0 = time.perf_counter()
-        o_s, _, _ = oa.sparse_attention(q, k, v, rp, ci, wl.block)
-        oa.reshape(o_s, rho[b:b + 1, h:h + 1], resid[b:b + 1, h:h + 1], 0.0)
-        t_total += time.perf_counter() - t0
-        done += 1
-        if t_total >= budget_s:
-            break
-    frac = done / len(heads)
-    return t_total, done, len(heads), frac, blas_threads
+    while t_total < budget_s:
+        for (b, h) in heads:
+            q = f(s2[0][b:b + 1, h:h + 1])
+            k = f(s2[1][b:b + 1, h:h + 1])
+            v = f(s2[2][b:b + 1, h:h + 1])
+            t0 = time.perf_counter()
+            o_s, _, _ = oa.sparse_attention(q, k, v, rp, ci, wl.block)
+            oa.reshape(o_s, rho[b:b + 1, h:h + 1], resid[b:b + 1, h:h + 1], 0.0)
+            t_total += time.perf_counter() - t0
+            done += 1
+            if t_total >= budget_s:
+                break
+    return t_total, done, len(heads), blas_threads
 
 
 def main():
@@ -317,7 +320,8 @@ def main():
     if not args.no_cpu_baseline:
         rho_h = rho.cpu().numpy().astype(np.float64)
         resid_h = resid.float().cpu().numpy().astype(np.float64)
-        t_cpu, done, total, frac, blas = cpu_baseline(wl, s2, rp, ci, rho_h, resid_h, args.cpu_budget)
+        t_cpu, done, total, blas = cpu_baseline(wl, s2, rp, ci, rho_h, resid_h, args.cpu_budget)
+        frac = done / total  # calls' worth of work timed (can exceed 1)
         cores = len(os.sched_getaffinity(0))
         cpu_tflops = flops * frac / t_cpu / 1e12
         cpu = {
@@ -326,8 +330,8 @@ def main():
             "cores": int(blas or cores),
             "host_cores": cores,
             "kind": "oracle",
-            "sample": f"{done} of {total} (batch, head) pairs, every query row; fp64 NumPy sparse "
-                      f"attention + reshape; {t_cpu:.1f} s",
+            "sample": f"{done} (batch, head) pair evaluations ({frac:.2f} calls' worth of the {total} "
+                      f"pairs), every query row; fp64 NumPy sparse attention + reshape; {t_cpu:.1f} s",
             "ms_per_call_extrapolated": t_cpu / frac * 1e3,
         }
         # the oracle's dense attention (Eq.1 / Eq.4) on one (batch, head) pair,
