@@ -17,8 +17,8 @@
 // exactly the 8+8 key values the B operand of the P V product needs, so P
 // never leaves registers.  The rows of the V^T operand are permuted so that
 // each lane's 16 accumulator values of O^T are 16 consecutive head dims of
-// its query: the residual rows are read and the output leaves as 16-byte
-// vector loads and stores straight from registers.
+// its query: a lane reads its residual values with 16-byte LDS reads and
+// stores its output rows with 16-byte stores straight from registers.
 //
 // Memory.  Q arrives by buffer loads straight into its B-operand registers.
 // K and V chunks move from HBM/L2 into LDS rings (three K stages, two V stages,
