@@ -16,8 +16,9 @@
  *    row_sum l = sum_j exp(A^pre_ij - m) over the keys the call attends to,
  *    so l * exp(m) is the softmax denominator of Eq.4 (dense) or Eq.5 (sparse).
  *  - rho is fp32 [B, H, T]; one value per batch element, head and query row.
- *  - The block mask is a CSR over blocks of `block` tokens shared by every
- *    (batch, head): block b covers tokens [b*block, min((b+1)*block, T)),
+ *  - The block mask is a CSR over blocks of `block` tokens, shared by every
+ *    (batch, head) or given per head (rt_bsr): block b covers tokens
+ *    [b*block, min((b+1)*block, T)),
  *    n_qblk = n_kblk = ceil(T / block).  row_ptr has n_qblk+1 entries, col_idx
  *    lists the kept key blocks of each query block in ascending order.  A key
  *    past T is never attended to.
