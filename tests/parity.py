@@ -13,6 +13,16 @@ BF16_REL_L2 = 1e-2
 STAT_REL = 1e-3
 
 
+def _log_margin(kind, what, value, bound):
+    """Appends one comparison to the file named by RT_PARITY_LOG, if set."""
+    import os
+
+    path = os.environ.get("RT_PARITY_LOG")
+    if path:
+        with open(path, "a") as f:
+            f.write(f"{kind}\t{value:.6e}\t{bound:.1e}\t{what}\n")
+
+
 def to_dev(bits, device="cuda"):
     import torch
 
@@ -42,6 +52,8 @@ def assert_bf16_close(got, ref, what=""):
     max_abs = float(np.max(np.abs(err))) if err.size else 0.0
     den = float(np.linalg.norm(ref))
     rel = float(np.linalg.norm(err)) / den if den > 0 else float(np.linalg.norm(err))
+    _log_margin("max_abs", what, max_abs, BF16_MAX_ABS)
+    _log_margin("rel_l2", what, rel, BF16_REL_L2)
     assert max_abs <= BF16_MAX_ABS, f"{what}: max-abs {max_abs:.3e} > {BF16_MAX_ABS}"
     assert rel <= BF16_REL_L2, f"{what}: rel-L2 {rel:.3e} > {BF16_REL_L2}"
     return max_abs, rel
@@ -55,6 +67,7 @@ def assert_stat_close(got, ref, what="", floor=0.0):
     scale = np.maximum(np.abs(ref), floor)
     rel = np.abs(got - ref) / np.where(scale > 0, scale, 1.0)
     worst = float(rel.max()) if rel.size else 0.0
+    _log_margin("stat_rel", what, worst, STAT_REL)
     assert worst <= STAT_REL, f"{what}: worst relative error {worst:.3e} > {STAT_REL}"
     return worst
 
