@@ -11,6 +11,11 @@ import numpy as np
 BF16_MAX_ABS = 2e-2
 BF16_REL_L2 = 1e-2
 STAT_REL = 1e-3
+# Relative L2 is measured against max(|ref|, this RMS): a reference below it is
+# zero up to fp64 rounding, e.g. R of a row that keeps every key (App. A.3:
+# R = A_{not in S} V = 0), where the kernel returns the exact 0 and the oracle's
+# Eq.10 subtraction leaves ~1e-16.  Real outputs here are ~1e-3 and above.
+REL_L2_FLOOR_RMS = 1e-9
 
 
 def _log_margin(kind, what, value, bound):
@@ -50,7 +55,7 @@ def assert_bf16_close(got, ref, what=""):
     assert np.all(np.isfinite(got)), f"{what}: non-finite output"
     err = got - ref
     max_abs = float(np.max(np.abs(err))) if err.size else 0.0
-    den = float(np.linalg.norm(ref))
+    den = max(float(np.linalg.norm(ref)), REL_L2_FLOOR_RMS * np.sqrt(ref.size))
     rel = float(np.linalg.norm(err)) / den if den > 0 else float(np.linalg.norm(err))
     _log_margin("max_abs", what, max_abs, BF16_MAX_ABS)
     _log_margin("rel_l2", what, rel, BF16_REL_L2)

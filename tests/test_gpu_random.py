@@ -21,7 +21,7 @@ from parity import assert_bf16_close, assert_stat_close, to_dev, to_np
 
 pytestmark = pytest.mark.gpu
 
-N_CASES = 24
+N_CASES = 64
 
 
 def _case(i):
