@@ -31,6 +31,9 @@
  *    the call then returns a non-zero rt_status and enqueues nothing.  A launch
  *    failure returns RT_EHIP.  rt_last_error() describes the last failure on
  *    the calling thread.
+ *  - An output buffer must not overlap any input buffer or another output of
+ *    the same call (RT_EINVAL): every work item reads all of a head's K and V
+ *    while others write their output rows.
  *  - A call with B*H*T == 0 checks its arguments and enqueues nothing.
  */
 #ifndef RETTENTION_H
@@ -60,11 +63,15 @@ typedef struct {
  * row_ptr [n_masks][n_qblk + 1] and col_idx [nnz] are device int32 arrays;
  * row_ptr entries are absolute offsets into col_idx (mask m's rows start at
  * row_ptr[m][0]).  Head h of batch b uses mask 0 (n_masks 0 or 1), mask h
- * (n_masks == H) or mask b*H + h (n_masks == B*H).  The kernels clamp row_ptr
- * entries to [0, nnz] and skip column indices outside [0, n_qblk), so a
- * malformed CSR cannot make them read out of bounds; a query block with no
- * kept key block is outside Eq.5 (empty denominator) and its rows come out as
- * NaN (rt_attn_cache handles it: rho = 0). */
+ * (n_masks == H) or mask b*H + h (n_masks == B*H).  Every query block must
+ * keep at least one key block: Eq.5 normalises over the kept keys, so an empty
+ * kept set has no softmax.  rt_bsr_check verifies a host copy of the CSR (the
+ * Python binding runs it on every CSR it copies to the device) and the index
+ * builder never emits an empty row.  The attention calls do not read the device
+ * arrays on the host; for a CSR the host has not checked, the kernels clamp
+ * row_ptr entries to [0, nnz] and skip column indices outside [0, n_qblk), so a
+ * malformed CSR cannot make them read out of bounds, and a query block left
+ * with no kept key block comes out as NaN rows (rt_attn_cache: rho = 0). */
 typedef struct {
     const int32_t* row_ptr;
     const int32_t* col_idx;
@@ -73,6 +80,16 @@ typedef struct {
     int32_t nnz;     /* entries in col_idx */
     int32_t n_masks; /* 0 or 1 (shared), H or B*H */
 } rt_bsr;
+
+/* Host only.  Checks a host copy of a block CSR before it is used on the
+ * device: host_row_ptr [n_masks][n_qblk + 1] and host_col_idx [nnz] mirror
+ * mask->row_ptr / mask->col_idx (the device pointers are not read).  Returns
+ * RT_EINVAL when a row is empty (Eq.5 needs a kept key), when offsets leave
+ * [0, nnz] or decrease, when a column index leaves [0, n_qblk) or a row is
+ * not strictly ascending, or when nnz differs from the largest last offset
+ * (row_ptr[n_qblk] for a single mask); RT_EUNSUPPORTED for a block size other
+ * than 32 or 64. */
+rt_status rt_bsr_check(const rt_bsr* mask, const int32_t* host_row_ptr, const int32_t* host_col_idx);
 
 /* Static mask patterns (Sec.3 static masks; App. A.4 local windows). */
 enum {
@@ -112,7 +129,8 @@ typedef struct {
  */
 
 /* Host only.  Writes the exact number of CSR entries rt_index_build produces.
- * EXPLICIT reads pattern->host_mask (host, n_masks x n_qblk x n_qblk).  Needs T >= 1,
+ * EXPLICIT reads pattern->host_mask (host, n_masks x n_qblk x n_qblk) and
+ * returns RT_EINVAL for a row without a kept block (Eq.5).  Needs T >= 1,
  * block in {32, 64}, grid sizes matching T (LOCAL2D: grid_h*grid_w == T;
  * VIDEO3D: n_text + frames*grid_h*grid_w == T), keep >= 1, n_qblk <= 4096. */
 rt_status rt_index_size(const rt_pattern* pattern, int32_t T, int32_t block, int32_t* nnz_out);
@@ -122,8 +140,10 @@ rt_status rt_index_size(const rt_pattern* pattern, int32_t T, int32_t block, int
  * n_masks * ceil(T/block) <= 32768.
  * For LOCAL2D / VIDEO3D the size is known on the host and a capacity below it
  * is RT_ECAPACITY.  EXPLICIT reads pattern->mask (device) and writes at most
- * `capacity` entries; it returns RT_ECAPACITY when pattern->host_mask is given
- * and needs more, otherwise the caller must size capacity to the mask. */
+ * `capacity` entries; when pattern->host_mask is given it is checked as in
+ * rt_index_size (RT_EINVAL for an empty row, RT_ECAPACITY when it needs more
+ * than capacity), otherwise the caller must size capacity to the mask and keep
+ * every row non-empty. */
 rt_status rt_index_build(const rt_pattern* pattern, int32_t T, int32_t block, int32_t* row_ptr,
                          int32_t* col_idx, int32_t capacity, void* stream);
 
@@ -189,6 +209,8 @@ rt_status rt_attn_sparse_reshape(const void* q, const void* k, const void* v, rt
                                  void* stream);
 
 /* The same reshape applied to an already computed sparse output (unfused):
+ * Eq.9 scales the sparse softmax output by the cached ratio, ramped by
+ * rho_delta as in Sec.4.2 and clamped to 1, and Eq.10 adds the cached residual:
  *   O = min(1, rho + rho_delta) * o_sparse + R
  * o_sparse, resid, o: device bf16 [B,H,T,D]; rho: device fp32 [B,H,T]. */
 rt_status rt_reshape_apply(const void* o_sparse, const float* rho, const void* resid,

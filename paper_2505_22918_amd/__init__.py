@@ -82,18 +82,44 @@ def _check_qkv(q, k, v):
     return _lib.RtDims(B, H, T, D)
 
 
-def _stat(t, shape, name):
+def _on_device(t, name, device):
+    """t must be a CUDA tensor, on `device` when one is given (a host or
+    foreign-device pointer must never reach a kernel)."""
     torch = _torch()
-    if t.dtype is not torch.float32 or t.shape != shape or not t.is_contiguous():
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise ValueError(f"{name} must be a CUDA tensor")
+    if device is not None and t.device != device:
+        raise ValueError(f"{name} is on {t.device}, expected {device}")
+
+
+def _stat(t, shape, name, device=None):
+    torch = _torch()
+    _on_device(t, name, device)
+    if t.dtype is not torch.float32 or tuple(t.shape) != tuple(shape) or not t.is_contiguous():
         raise ValueError(f"{name} must be a contiguous fp32 tensor of shape {tuple(shape)}")
     return t
 
 
-def _bf16(t, shape, name):
+def _bf16(t, shape, name, device=None):
     torch = _torch()
-    if t.dtype is not torch.bfloat16 or t.shape != shape or not t.is_contiguous():
+    _on_device(t, name, device)
+    if t.dtype is not torch.bfloat16 or tuple(t.shape) != tuple(shape) or not t.is_contiguous():
         raise ValueError(f"{name} must be a contiguous bf16 tensor of shape {tuple(shape)}")
     return t
+
+
+def _out(out, like):
+    """A caller-supplied output tensor checked against `like` (shape, dtype,
+    contiguity, device), or a new one."""
+    if out is None:
+        return _torch().empty_like(like)
+    return _bf16(out, like.shape, "out", like.device)
+
+
+def _mask_on(mask, device):
+    """The mask's device arrays must sit on the device of the attention inputs."""
+    for name, t in (("mask.row_ptr", mask.row_ptr), ("mask.col_idx", mask.col_idx)):
+        _on_device(t, name, device)
 
 
 @dataclass(frozen=True)
@@ -120,11 +146,26 @@ class BlockMask:
 
     @classmethod
     def from_csr(cls, row_ptr, col_idx, block, device="cuda", n_masks=1):
-        """Copies a host CSR (numpy / lists) to the device as-is."""
+        """Checks a host CSR (numpy / lists) with rt_bsr_check, then copies it to
+        the device.  An empty row (Eq.5 needs a kept key), offsets outside
+        [0, nnz], column indices outside [0, n_qblk), unsorted rows or an nnz that
+        disagrees with the last offset raise RettentionError."""
+        import numpy as np
+
         torch = _torch()
-        rp = torch.as_tensor(row_ptr, dtype=torch.int32).to(device).contiguous()
-        ci = torch.as_tensor(col_idx, dtype=torch.int32).to(device).contiguous()
-        return cls(rp, ci, int(block), int(rp.numel()) // int(n_masks) - 1, int(ci.numel()), int(n_masks))
+        hrp = np.ascontiguousarray(np.asarray(row_ptr, dtype=np.int32).reshape(-1))
+        hci = np.ascontiguousarray(np.asarray(col_idx, dtype=np.int32).reshape(-1))
+        n_masks = int(n_masks)
+        if n_masks < 1 or hrp.size % n_masks or hrp.size // n_masks < 1:
+            raise ValueError(f"row_ptr of {hrp.size} entries does not hold {n_masks} masks")
+        n_qblk = hrp.size // n_masks - 1
+        c = _lib.RtBsr(None, None, int(block), n_qblk, int(hci.size), n_masks)
+        lib = _lib.load()
+        _lib.check("rt_bsr_check", lib.rt_bsr_check(ctypes.byref(c), hrp.ctypes.data if hrp.size else None,
+                                                    hci.ctypes.data if hci.size else None))
+        rp = torch.from_numpy(hrp).to(device).contiguous()
+        ci = torch.from_numpy(hci).to(device).contiguous()
+        return cls(rp, ci, int(block), n_qblk, int(hci.size), n_masks)
 
 
 def _pattern(kind, grid_h=0, grid_w=0, frames=0, n_text=0, keep=0, mask=None, host_mask=None, n_masks=1):
@@ -184,7 +225,7 @@ def attn_full(q, k, v, block=64, stats=True, out=None):
     torch = _torch()
     lib = _lib.load()
     dims = _check_qkv(q, k, v)
-    o = out if out is not None else torch.empty_like(q)
+    o = _out(out, q)
     m = l = None
     if stats:
         m = torch.empty(q.shape[:3], dtype=torch.float32, device=q.device)
@@ -199,7 +240,8 @@ def attn_sparse(q, k, v, mask: BlockMask, stats=True, out=None):
     torch = _torch()
     lib = _lib.load()
     dims = _check_qkv(q, k, v)
-    o = out if out is not None else torch.empty_like(q)
+    _mask_on(mask, q.device)
+    o = _out(out, q)
     m = l = None
     if stats:
         m = torch.empty(q.shape[:3], dtype=torch.float32, device=q.device)
@@ -216,7 +258,8 @@ def attn_cache(q, k, v, mask: BlockMask, stats=True, out=None):
     torch = _torch()
     lib = _lib.load()
     dims = _check_qkv(q, k, v)
-    o = out if out is not None else torch.empty_like(q)
+    _mask_on(mask, q.device)
+    o = _out(out, q)
     rho = torch.empty(q.shape[:3], dtype=torch.float32, device=q.device)
     resid = torch.empty_like(q)
     m = l = None
@@ -234,7 +277,8 @@ def attn_postmask(q, k, v, mask: BlockMask, out=None):
     torch = _torch()
     lib = _lib.load()
     dims = _check_qkv(q, k, v)
-    o = out if out is not None else torch.empty_like(q)
+    _mask_on(mask, q.device)
+    o = _out(out, q)
     bsr = mask.c_struct()
     _lib.check("rt_attn_postmask", lib.rt_attn_postmask(_ptr(q), _ptr(k), _ptr(v), dims, ctypes.byref(bsr),
                                                         _ptr(o), _stream(q)))
@@ -245,11 +289,15 @@ def cache_build(o_full, m_full, l_full, o_sparse, m_sparse, l_sparse):
     """rho (Eq.8) and residual R (Eq.10) at a caching step."""
     torch = _torch()
     lib = _lib.load()
+    _on_device(o_full, "o_full", None)
+    dev = o_full.device
+    if o_full.dim() != 4:
+        raise ValueError("o_full must be a bf16 [B,H,T,D] tensor")
     B, H, T, D = o_full.shape
-    _bf16(o_full, o_full.shape, "o_full")
-    _bf16(o_sparse, o_full.shape, "o_sparse")
+    _bf16(o_full, o_full.shape, "o_full", dev)
+    _bf16(o_sparse, o_full.shape, "o_sparse", dev)
     for name, t in (("m_full", m_full), ("l_full", l_full), ("m_sparse", m_sparse), ("l_sparse", l_sparse)):
-        _stat(t, (B, H, T), name)
+        _stat(t, (B, H, T), name, dev)
     rho = torch.empty((B, H, T), dtype=torch.float32, device=o_full.device)
     resid = torch.empty_like(o_full)
     _lib.check("rt_cache_build", lib.rt_cache_build(_ptr(o_full), _ptr(m_full), _ptr(l_full), _ptr(o_sparse),
@@ -263,9 +311,10 @@ def attn_sparse_reshape(q, k, v, mask: BlockMask, rho, resid, rho_delta=0.0, sta
     torch = _torch()
     lib = _lib.load()
     dims = _check_qkv(q, k, v)
-    _stat(rho, q.shape[:3], "rho")
-    _bf16(resid, q.shape, "resid")
-    o = out if out is not None else torch.empty_like(q)
+    _mask_on(mask, q.device)
+    _stat(rho, q.shape[:3], "rho", q.device)
+    _bf16(resid, q.shape, "resid", q.device)
+    o = _out(out, q)
     m = l = None
     if stats:
         m = torch.empty(q.shape[:3], dtype=torch.float32, device=q.device)
@@ -281,11 +330,15 @@ def reshape_apply(o_sparse, rho, resid, rho_delta=0.0, out=None):
     """Unfused Eq.9 + Eq.10 on a sparse output: min(1, rho + delta) * o_sparse + R."""
     torch = _torch()
     lib = _lib.load()
+    _on_device(o_sparse, "o_sparse", None)
+    dev = o_sparse.device
+    if o_sparse.dim() != 4:
+        raise ValueError("o_sparse must be a bf16 [B,H,T,D] tensor")
     B, H, T, D = o_sparse.shape
-    _bf16(o_sparse, o_sparse.shape, "o_sparse")
-    _bf16(resid, o_sparse.shape, "resid")
-    _stat(rho, (B, H, T), "rho")
-    o = out if out is not None else torch.empty_like(o_sparse)
+    _bf16(o_sparse, o_sparse.shape, "o_sparse", dev)
+    _bf16(resid, o_sparse.shape, "resid", dev)
+    _stat(rho, (B, H, T), "rho", dev)
+    o = _out(out, o_sparse)
     _lib.check("rt_reshape_apply", lib.rt_reshape_apply(_ptr(o_sparse), _ptr(rho), _ptr(resid), float(rho_delta),
                                                         _lib.RtDims(B, H, T, D), _ptr(o), _stream(o_sparse)))
     return o

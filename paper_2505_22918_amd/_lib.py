@@ -52,6 +52,7 @@ class RtPattern(ctypes.Structure):
 
 
 _SIGS = {
+    "rt_bsr_check": (c_int32, [ctypes.POINTER(RtBsr), c_void_p, c_void_p]),
     "rt_index_size": (c_int32, [ctypes.POINTER(RtPattern), c_int32, c_int32, ctypes.POINTER(c_int32)]),
     "rt_index_build": (c_int32, [ctypes.POINTER(RtPattern), c_int32, c_int32, c_void_p, c_void_p,
                                  c_int32, c_void_p]),

@@ -7,7 +7,10 @@
 #include <cstdarg>
 #include <cstdint>
 #include <cstdio>
+#include <algorithm>
+#include <initializer_list>
 #include <numeric>
+#include <utility>
 
 #include "../../include/rettention.h"
 #include "kernels.h"
@@ -80,6 +83,40 @@ rt_status check_qkv(const void* q, const void* k, const void* v, void* o) {
     RT_TRY(check_tensor(k, "k"));
     RT_TRY(check_tensor(v, "v"));
     RT_TRY(check_tensor(o, "o"));
+    return RT_OK;
+}
+
+int64_t tensor_bytes(const rt_dims& d, int64_t elem) { return (int64_t)d.B * d.H * d.T * d.D * elem; }
+
+// The byte ranges [a, a + na) and [b, b + nb) share a byte.
+bool overlaps(const void* a, int64_t na, const void* b, int64_t nb) {
+    const uintptr_t x = reinterpret_cast<uintptr_t>(a), y = reinterpret_cast<uintptr_t>(b);
+    return x < y + (uintptr_t)nb && y < x + (uintptr_t)na;
+}
+
+// Attention outputs are written by one work item per query block while every
+// work item reads K and V (and its own Q rows), so an output that overlaps an
+// input would be read back by other work items; no overlap is accepted.
+rt_status check_no_overlap(const void* out, int64_t out_bytes, const char* out_name,
+                           std::initializer_list<std::pair<const void*, int64_t>> ins, const char* in_names) {
+    for (const auto& in : ins)
+        if (in.first && overlaps(out, out_bytes, in.first, in.second))
+            return fail(RT_EINVAL, "%s overlaps %s (outputs must not alias the inputs)", out_name, in_names);
+    return RT_OK;
+}
+
+// Optional row statistics: they must not overlap each other, o or the other
+// listed buffers.
+rt_status check_stats_overlap(const rt_dims& d, const float* row_max, const float* row_sum, const void* o,
+                              std::initializer_list<std::pair<const void*, int64_t>> others) {
+    const int64_t ns = tensor_bytes(d, 4) / d.D, nt = tensor_bytes(d, 2);
+    for (const float* st : {row_max, row_sum}) {
+        if (!st) continue;
+        RT_TRY(check_no_overlap(st, ns, "row_max / row_sum", {{o, nt}}, "o"));
+        RT_TRY(check_no_overlap(st, ns, "row_max / row_sum", others, "another output or input"));
+    }
+    if (row_max && row_sum && overlaps(row_max, ns, row_sum, ns))
+        return fail(RT_EINVAL, "row_max overlaps row_sum");
     return RT_OK;
 }
 
@@ -226,8 +263,17 @@ rt_status rt_index_size(const rt_pattern* pattern, int32_t T, int32_t block, int
     if (pattern->kind == RT_PAT_EXPLICIT) {
         if (!pattern->host_mask) return fail(RT_EINVAL, "EXPLICIT pattern needs host_mask for sizing");
         nnz = 0;
-        const int64_t cells = (int64_t)a.n_masks * a.n_blk * a.n_blk;
-        for (int64_t i = 0; i < cells; ++i) nnz += pattern->host_mask[i] != 0;
+        const int64_t rows = (int64_t)a.n_masks * a.n_blk;
+        for (int64_t r = 0; r < rows; ++r) {
+            const uint8_t* row = pattern->host_mask + r * a.n_blk;
+            int64_t kept = 0;
+            for (int64_t j = 0; j < a.n_blk; ++j) kept += row[j] != 0;
+            // Eq.5 normalises over the kept keys: an empty kept set has no softmax
+            if (kept == 0)
+                return fail(RT_EINVAL, "mask %lld, query block %lld keeps no key block (Eq.5 needs one)",
+                            (long long)(r / a.n_blk), (long long)(r % a.n_blk));
+            nnz += kept;
+        }
     }
     if (nnz > INT32_MAX) return fail(RT_EINVAL, "nnz exceeds int32");
     *nnz_out = (int32_t)nnz;
@@ -258,6 +304,42 @@ rt_status rt_index_build(const rt_pattern* pattern, int32_t T, int32_t block, in
     return hip_status(rt::launch_index_build(a, static_cast<hipStream_t>(stream)), "index build launch");
 }
 
+rt_status rt_bsr_check(const rt_bsr* mask, const int32_t* host_row_ptr, const int32_t* host_col_idx) {
+    if (!mask) return fail(RT_EINVAL, "mask is NULL");
+    RT_TRY(check_block(mask->block));
+    if (mask->n_qblk < 0 || mask->nnz < 0 || mask->n_masks < 0)
+        return fail(RT_EINVAL, "n_qblk=%d nnz=%d n_masks=%d", mask->n_qblk, mask->nnz, mask->n_masks);
+    const int64_t nb = mask->n_qblk, nm = mask->n_masks > 1 ? mask->n_masks : 1;
+    if (nb == 0) return mask->nnz == 0 ? ok() : fail(RT_EINVAL, "nnz=%d for a mask without rows", mask->nnz);
+    if (!host_row_ptr || !host_col_idx) return fail(RT_EINVAL, "host_row_ptr / host_col_idx is NULL");
+    int64_t last = 0;
+    for (int64_t m = 0; m < nm; ++m) {
+        const int32_t* rp = host_row_ptr + m * (nb + 1);
+        for (int64_t i = 0; i < nb; ++i) {
+            if (rp[i] < 0 || rp[i + 1] > mask->nnz)
+                return fail(RT_EINVAL, "mask %lld row %lld: offsets [%d, %d) outside [0, nnz=%d]", (long long)m,
+                            (long long)i, rp[i], rp[i + 1], mask->nnz);
+            // Eq.5 normalises over the kept keys: an empty kept set has no softmax
+            if (rp[i + 1] <= rp[i])
+                return fail(RT_EINVAL, "mask %lld, query block %lld keeps no key block (Eq.5 needs one)",
+                            (long long)m, (long long)i);
+            for (int32_t e = rp[i]; e < rp[i + 1]; ++e) {
+                const int32_t c = host_col_idx[e];
+                if (c < 0 || c >= nb)
+                    return fail(RT_EINVAL, "mask %lld row %lld: key block %d outside [0, %lld)", (long long)m,
+                                (long long)i, c, (long long)nb);
+                if (e > rp[i] && c <= host_col_idx[e - 1])
+                    return fail(RT_EINVAL, "mask %lld row %lld: key blocks not strictly ascending", (long long)m,
+                                (long long)i);
+            }
+        }
+        last = std::max<int64_t>(last, rp[nb]);
+    }
+    if (last != mask->nnz)
+        return fail(RT_EINVAL, "nnz=%d but the row offsets end at %lld", mask->nnz, (long long)last);
+    return ok();
+}
+
 rt_status rt_attn_full(const void* q, const void* k, const void* v, rt_dims dims, int32_t block, void* o,
                        float* row_max, float* row_sum, void* stream) {
     bool empty = false;
@@ -267,6 +349,9 @@ rt_status rt_attn_full(const void* q, const void* k, const void* v, rt_dims dims
     RT_TRY(check_qkv(q, k, v, o));
     if (row_max) RT_TRY(check_stat(row_max, "row_max"));
     if (row_sum) RT_TRY(check_stat(row_sum, "row_sum"));
+    const int64_t nt = tensor_bytes(dims, 2);
+    RT_TRY(check_no_overlap(o, nt, "o", {{q, nt}, {k, nt}, {v, nt}}, "q, k or v"));
+    RT_TRY(check_stats_overlap(dims, row_max, row_sum, o, {}));
     RT_TRY(check_items(dims, block));
     rt::AttnArgs a = base_args(q, k, v, dims, block, o, row_max, row_sum);
     a.dense = 1;
@@ -283,6 +368,9 @@ rt_status rt_attn_sparse(const void* q, const void* k, const void* v, rt_dims di
     RT_TRY(check_qkv(q, k, v, o));
     if (row_max) RT_TRY(check_stat(row_max, "row_max"));
     if (row_sum) RT_TRY(check_stat(row_sum, "row_sum"));
+    const int64_t nt = tensor_bytes(dims, 2);
+    RT_TRY(check_no_overlap(o, nt, "o", {{q, nt}, {k, nt}, {v, nt}}, "q, k or v"));
+    RT_TRY(check_stats_overlap(dims, row_max, row_sum, o, {}));
     RT_TRY(check_items(dims, mask->block));
     rt::AttnArgs a = base_args(q, k, v, dims, mask->block, o, row_max, row_sum);
     set_mask(a, mask, dims);
@@ -301,8 +389,12 @@ rt_status rt_attn_cache(const void* q, const void* k, const void* v, rt_dims dim
     RT_TRY(check_tensor(resid, "resid"));
     if (row_max) RT_TRY(check_stat(row_max, "row_max"));
     if (row_sum) RT_TRY(check_stat(row_sum, "row_sum"));
-    if (resid == o || resid == q || resid == k || resid == v || o == q || o == k || o == v)
-        return fail(RT_EINVAL, "o and resid must not alias q, k, v or each other");
+    const int64_t nt = tensor_bytes(dims, 2), ns = tensor_bytes(dims, 4) / dims.D;
+    RT_TRY(check_no_overlap(o, nt, "o", {{q, nt}, {k, nt}, {v, nt}, {resid, nt}}, "q, k, v or resid"));
+    RT_TRY(check_no_overlap(resid, nt, "resid", {{q, nt}, {k, nt}, {v, nt}}, "q, k or v"));
+    RT_TRY(check_no_overlap(rho, ns, "rho", {{q, nt}, {k, nt}, {v, nt}, {o, nt}, {resid, nt}},
+                            "q, k, v, o or resid"));
+    RT_TRY(check_stats_overlap(dims, row_max, row_sum, o, {{resid, nt}, {rho, ns}}));
     RT_TRY(check_items(dims, mask->block));
     rt::AttnArgs a = base_args(q, k, v, dims, mask->block, o, row_max, row_sum);
     set_mask(a, mask, dims);
@@ -319,7 +411,8 @@ rt_status rt_attn_postmask(const void* q, const void* k, const void* v, rt_dims 
     RT_TRY(check_bsr(mask, dims));
     if (empty) return ok();
     RT_TRY(check_qkv(q, k, v, o));
-    if (o == q || o == k || o == v) return fail(RT_EINVAL, "o must not alias q, k or v");
+    const int64_t nt = tensor_bytes(dims, 2);
+    RT_TRY(check_no_overlap(o, nt, "o", {{q, nt}, {k, nt}, {v, nt}}, "q, k or v"));
     RT_TRY(check_items(dims, mask->block));
     rt::AttnArgs a = base_args(q, k, v, dims, mask->block, o, nullptr, nullptr);
     set_mask(a, mask, dims);
@@ -342,6 +435,14 @@ rt_status rt_cache_build(const void* o_full, const float* m_full, const float* l
     RT_TRY(check_stat(m_sparse, "m_sparse"));
     RT_TRY(check_stat(l_sparse, "l_sparse"));
     RT_TRY(check_stat(rho, "rho"));
+    {
+        const int64_t nt = tensor_bytes(dims, 2), ns = tensor_bytes(dims, 4) / dims.D;
+        const std::initializer_list<std::pair<const void*, int64_t>> ins = {
+            {o_full, nt}, {o_sparse, nt}, {m_full, ns}, {l_full, ns}, {m_sparse, ns}, {l_sparse, ns}};
+        RT_TRY(check_no_overlap(resid, nt, "resid", ins, "an input"));
+        RT_TRY(check_no_overlap(rho, ns, "rho", ins, "an input"));
+        RT_TRY(check_no_overlap(rho, ns, "rho", {{resid, nt}}, "resid"));
+    }
     const int64_t rows = (int64_t)dims.B * dims.H * dims.T;
     return hip_status(rt::launch_cache_build(static_cast<const uint16_t*>(o_full), m_full, l_full,
                                              static_cast<const uint16_t*>(o_sparse), m_sparse, l_sparse, rows,
@@ -363,6 +464,10 @@ rt_status rt_attn_sparse_reshape(const void* q, const void* k, const void* v, rt
     RT_TRY(check_tensor(resid, "resid"));
     if (row_max) RT_TRY(check_stat(row_max, "row_max"));
     if (row_sum) RT_TRY(check_stat(row_sum, "row_sum"));
+    const int64_t nt = tensor_bytes(dims, 2), ns = tensor_bytes(dims, 4) / dims.D;
+    RT_TRY(check_no_overlap(o, nt, "o", {{q, nt}, {k, nt}, {v, nt}, {resid, nt}, {rho, ns}},
+                            "q, k, v, resid or rho"));
+    RT_TRY(check_stats_overlap(dims, row_max, row_sum, o, {{resid, nt}, {rho, ns}}));
     RT_TRY(check_items(dims, mask->block));
     rt::AttnArgs a = base_args(q, k, v, dims, mask->block, o, row_max, row_sum);
     set_mask(a, mask, dims);
@@ -383,6 +488,10 @@ rt_status rt_reshape_apply(const void* o_sparse, const float* rho, const void* r
     RT_TRY(check_tensor(resid, "resid"));
     RT_TRY(check_tensor(o, "o"));
     RT_TRY(check_stat(rho, "rho"));
+    {
+        const int64_t nt = tensor_bytes(dims, 2), ns = tensor_bytes(dims, 4) / dims.D;
+        RT_TRY(check_no_overlap(o, nt, "o", {{o_sparse, nt}, {resid, nt}, {rho, ns}}, "o_sparse, resid or rho"));
+    }
     const int64_t rows = (int64_t)dims.B * dims.H * dims.T;
     return hip_status(rt::launch_reshape_apply(static_cast<const uint16_t*>(o_sparse), rho,
                                                static_cast<const uint16_t*>(resid), rho_delta, rows, dims.D,

@@ -5,10 +5,12 @@ steps (5 for the PixArt models, 10 for Hunyuan, 15 for CogVideoX), then sparse
 attention with a full-attention caching step every 5 steps; Sec.4.2 ramps the
 cached ratio by lambda per step between caching steps.  ``StatCache`` holds one
 layer's cache; ``run`` drives a whole synthetic run in which Q, K and V drift
-by sigma * N(0, 1) per step, and can report, per step, how far the ramped cached
-ratio is from the ratio measured on that step's inputs and how far the reshaped
-and the plainly sparse outputs are from full attention (the paper tracks the
-same ratio over steps for single tokens).
+by sigma * N(0, 1) per step, and can report, per step, how far the cached ratio
+has drifted from the ratio measured on that step's inputs and how far the
+reshaped and the plainly sparse outputs are from full attention (the paper
+tracks the same ratio over steps for single tokens).  Every number is a library
+output or a plain difference of two: the ramp and clamp of Eq.9 run only inside
+the library's fused call, whose output error is what shows the ramp's effect.
 
     python -m paper_2505_22918_amd.schedule --workload cogvideox_2b --steps 50 \\
         --full-steps 15 --period 5 --lam 0.0 --sigma 0.02
@@ -71,12 +73,13 @@ def run(mask, qkv, n_steps, full_steps, period, lam, sigma, seed=0, diagnose=Tru
             if caching:
                 rec["out_rel_err_vs_full"] = 0.0
             else:
-                applied = torch.clamp(cache.rho + rec["rho_delta"], max=1.0)
-                diff = applied - rho_t
-                rec["rho_applied_mean"] = float(applied.mean())
-                rec["rho_abs_err_mean"] = float(diff.abs().mean())
-                rec["rho_abs_err_max"] = float(diff.abs().max())
-                rec["rho_err_signed_mean"] = float(diff.mean())
+                # drift of the cached ratio (from the last caching step) against the
+                # ratio of this step's inputs
+                drift = cache.rho - rho_t
+                rec["rho_cached_mean"] = float(cache.rho.mean())
+                rec["rho_drift_abs_mean"] = float(drift.abs().mean())
+                rec["rho_drift_abs_max"] = float(drift.abs().max())
+                rec["rho_drift_signed_mean"] = float(drift.mean())
                 o_s = attn_sparse(q, k, v, mask, stats=False)
                 rec["out_rel_err_vs_full"] = float(torch.linalg.vector_norm(out.float() - o_f.float()) / nf)
                 rec["sparse_rel_err_vs_full"] = float(torch.linalg.vector_norm(o_s.float() - o_f.float()) / nf)
@@ -120,7 +123,7 @@ def main(argv=None):
         "lam": args.lam, "sigma": args.sigma,
         "caching_steps": sum(1 for r in recs if r["kind"] != "reshape"),
         "reshape_steps": len(rs),
-        "mean_rho_abs_err": float(np.mean([r["rho_abs_err_mean"] for r in rs])) if rs else None,
+        "mean_rho_drift_abs": float(np.mean([r["rho_drift_abs_mean"] for r in rs])) if rs else None,
         "mean_out_rel_err_reshape": float(np.mean([r["out_rel_err_vs_full"] for r in rs])) if rs else None,
         "mean_out_rel_err_sparse": float(np.mean([r["sparse_rel_err_vs_full"] for r in rs])) if rs else None,
     }

@@ -12,6 +12,10 @@ from paper_2505_22918_amd import _lib, synth
 import paper_2505_22918_amd as rt
 
 FAKE = 0x7F0000000000  # 16-byte aligned, never dereferenced: every call below fails validation first
+# distinct fake tensors of the default test shape (64 KiB each, 1 MiB apart), so a
+# call fails on the one condition a test plants and not on aliasing
+Q, K, V, O, O2 = (FAKE + i * 0x100000 for i in range(5))
+S1, S2, S3, S4, S5 = (FAKE + 0x1000000 + i * 0x100000 for i in range(5))  # fp32 [B,H,T] slots
 
 
 @pytest.fixture(scope="module")
@@ -133,18 +137,23 @@ def test_attention_argument_errors(lib):
     assert st(FAKE, FAKE, FAKE, d, ctypes.byref(_bsr(block=16)), FAKE, None, None, None) == _lib.RT_EUNSUPPORTED
     assert st(FAKE, FAKE, FAKE, d, ctypes.byref(_bsr(nnz=0)), FAKE, None, None, None) == _lib.RT_EINVAL
     assert st(FAKE, FAKE, FAKE, d, ctypes.byref(_bsr(rp=None)), FAKE, None, None, None) == _lib.RT_EINVAL
-    assert st(FAKE, FAKE, FAKE, d, ctypes.byref(b), FAKE, FAKE + 2, None, None) == _lib.RT_EINVAL
+    assert st(Q, K, V, d, ctypes.byref(b), O, S1 + 2, None, None) == _lib.RT_EINVAL
+    assert "aligned" in lib.rt_last_error().decode()
     full = lib.rt_attn_full
     assert full(FAKE, FAKE, FAKE, d, 48, FAKE, None, None, None) == _lib.RT_EUNSUPPORTED
     assert full(FAKE, None, FAKE, d, 64, FAKE, None, None, None) == _lib.RT_EINVAL
     rs = lib.rt_attn_sparse_reshape
-    assert rs(FAKE, FAKE, FAKE, d, ctypes.byref(b), None, FAKE, 0.0, FAKE, None, None, None) == _lib.RT_EINVAL
-    assert rs(FAKE, FAKE, FAKE, d, ctypes.byref(b), FAKE, None, 0.0, FAKE, None, None, None) == _lib.RT_EINVAL
-    assert rs(FAKE, FAKE, FAKE, d, ctypes.byref(b), FAKE, FAKE, float("nan"), FAKE, None, None,
-              None) == _lib.RT_EINVAL
+    assert rs(Q, K, V, d, ctypes.byref(b), None, O2, 0.0, O, None, None, None) == _lib.RT_EINVAL
+    assert "rho" in lib.rt_last_error().decode()
+    assert rs(Q, K, V, d, ctypes.byref(b), S1, None, 0.0, O, None, None, None) == _lib.RT_EINVAL
+    assert "resid" in lib.rt_last_error().decode()
+    assert rs(Q, K, V, d, ctypes.byref(b), S1, O2, float("nan"), O, None, None, None) == _lib.RT_EINVAL
+    assert "rho_delta" in lib.rt_last_error().decode()
     ra = lib.rt_reshape_apply
-    assert ra(FAKE, FAKE, FAKE, float("inf"), d, FAKE, None) == _lib.RT_EINVAL
-    assert ra(FAKE, None, FAKE, 0.0, d, FAKE, None) == _lib.RT_EINVAL
+    assert ra(Q, S1, K, float("inf"), d, O, None) == _lib.RT_EINVAL
+    assert "rho_delta" in lib.rt_last_error().decode()
+    assert ra(Q, None, K, 0.0, d, O, None) == _lib.RT_EINVAL
+    assert "rho" in lib.rt_last_error().decode()
     ac = lib.rt_attn_cache
     other = FAKE + 0x100000
     assert ac(FAKE, FAKE, FAKE, d, ctypes.byref(b), other, None, None, None, FAKE + 0x200000, None) == _lib.RT_EINVAL
@@ -161,7 +170,8 @@ def test_attention_argument_errors(lib):
     assert pm(FAKE, FAKE, FAKE, d, ctypes.byref(b), None, None) == _lib.RT_EINVAL
     assert pm(FAKE, FAKE, FAKE, d, None, FAKE + 0x100000, None) == _lib.RT_EINVAL
     cb = lib.rt_cache_build
-    assert cb(FAKE, FAKE, FAKE, FAKE, FAKE, None, d, FAKE, FAKE, None) == _lib.RT_EINVAL
+    assert cb(Q, S1, S2, K, S3, None, d, S5, O, None) == _lib.RT_EINVAL
+    assert "l_sparse" in lib.rt_last_error().decode()
     assert cb(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, _dims(D=80), FAKE, FAKE, None) == _lib.RT_EUNSUPPORTED
 
 
@@ -202,3 +212,123 @@ def test_empty_problem_is_a_no_op(lib):
     assert lib.rt_attn_cache(None, None, None, _dims(T=0), ctypes.byref(b), None, None, None, None, None,
                              None) == _lib.RT_OK
     assert lib.rt_last_error().decode() == ""
+
+
+def _csr_status(lib, rp, ci, block=64, n_qblk=None, nnz=None, n_masks=1):
+    rp = np.ascontiguousarray(rp, dtype=np.int32)
+    ci = np.ascontiguousarray(ci, dtype=np.int32)
+    nq = (rp.size // max(n_masks, 1) - 1) if n_qblk is None else n_qblk
+    b = _lib.RtBsr(None, None, block, nq, ci.size if nnz is None else nnz, n_masks)
+    return lib.rt_bsr_check(ctypes.byref(b), rp.ctypes.data if rp.size else None,
+                            ci.ctypes.data if ci.size else None)
+
+
+def test_bsr_check_accepts_well_formed_masks(lib):
+    # the workloads' own CSRs, and a stacked per-head pair
+    for name in synth.WORKLOADS:
+        wl = synth.WORKLOADS[name]
+        if wl.kind == synth.PAT_EXPLICIT:
+            rp, ci = ob.block_index_explicit(synth.explicit_block_mask(wl.n_blk, wl.seed))
+        elif wl.kind == synth.PAT_LOCAL2D:
+            rp, ci = ob.block_index_local2d(wl.T, wl.block, wl.grid_h, wl.grid_w, wl.keep)
+        else:
+            rp, ci = ob.block_index_video3d(wl.T, wl.block, wl.n_text, wl.frames, wl.grid_h, wl.grid_w, wl.keep)
+        assert _csr_status(lib, rp, ci, block=wl.block) == _lib.RT_OK, name
+    assert _csr_status(lib, [0, 1, 3, 3, 5, 6], [0, 0, 1, 1, 0, 1][:6], n_masks=2, n_qblk=2, nnz=6) in (
+        _lib.RT_EINVAL,)  # second mask starts at 3 but its first row is empty (3 -> 3)
+    assert _csr_status(lib, [0, 1, 3, 3, 4, 6], [0, 0, 1, 0, 0, 1], n_masks=2, n_qblk=2) == _lib.RT_OK
+    assert lib.rt_last_error().decode() == ""
+
+
+@pytest.mark.parametrize("rp, ci, nnz, needle", [
+    ([0, 1, 1, 3], [0, 1, 2], None, "keeps no key block"),       # empty row (Eq.5)
+    ([0, 2, 3, 4], [0, 1, 2, 2], 5, "nnz=5"),                      # nnz beyond the last offset
+    ([0, 2, 3, 5], [0, 1, 2, 0, 2], 4, "outside"),                 # offset past nnz
+    ([0, 2, 1, 3], [0, 1, 2], None, "keeps no key block"),       # offsets decrease
+    ([-1, 1, 2, 3], [0, 1, 2], None, "outside"),                   # negative offset
+    ([0, 1, 2, 3], [0, 3, 2], None, "outside [0, 3)"),             # column index past n_qblk
+    ([0, 1, 2, 3], [0, -1, 2], None, "outside [0, 3)"),            # negative column index
+    ([0, 2, 3, 4], [1, 0, 1, 2], None, "ascending"),               # unsorted row
+    ([0, 2, 3, 4], [1, 1, 1, 2], None, "ascending"),               # repeated column
+])
+def test_bsr_check_rejects(lib, rp, ci, nnz, needle):
+    assert _csr_status(lib, rp, ci, nnz=nnz) == _lib.RT_EINVAL
+    assert needle in lib.rt_last_error().decode()
+
+
+def test_bsr_check_argument_errors(lib):
+    b = _lib.RtBsr(None, None, 48, 2, 2, 1)
+    rp = np.array([0, 1, 2], np.int32)
+    ci = np.array([0, 1], np.int32)
+    assert lib.rt_bsr_check(ctypes.byref(b), rp.ctypes.data, ci.ctypes.data) == _lib.RT_EUNSUPPORTED
+    b = _lib.RtBsr(None, None, 64, 2, 2, 1)
+    assert lib.rt_bsr_check(None, rp.ctypes.data, ci.ctypes.data) == _lib.RT_EINVAL
+    assert lib.rt_bsr_check(ctypes.byref(b), None, ci.ctypes.data) == _lib.RT_EINVAL
+    assert lib.rt_bsr_check(ctypes.byref(b), rp.ctypes.data, None) == _lib.RT_EINVAL
+    b = _lib.RtBsr(None, None, 64, 0, 0, 1)  # no rows, no entries: nothing to check
+    assert lib.rt_bsr_check(ctypes.byref(b), None, None) == _lib.RT_OK
+
+
+def test_blockmask_from_csr_checks_on_the_host(lib):
+    # rejected before anything is copied (no device needed)
+    with pytest.raises(rt.RettentionError, match="keeps no key block"):
+        rt.BlockMask.from_csr([0, 1, 1, 3], [0, 1, 2], 64, device="cpu")
+    with pytest.raises(rt.RettentionError, match="nnz=4"):
+        rt.BlockMask.from_csr([0, 1, 2, 3], [0, 1, 2, 0], 64, device="cpu")  # col_idx longer than the rows
+    with pytest.raises(ValueError, match="masks"):
+        rt.BlockMask.from_csr([0, 1, 2], [0, 1], 64, device="cpu", n_masks=2)
+
+
+def test_explicit_mask_with_an_empty_row_is_rejected(lib):
+    n = ctypes.c_int32()
+    hm = np.eye(4, dtype=np.uint8)
+    hm[2, 2] = 0
+    p = _pat(kind=0, mask=FAKE, host_mask=hm.ctypes.data)
+    assert lib.rt_index_size(ctypes.byref(p), 256, 64, ctypes.byref(n)) == _lib.RT_EINVAL
+    assert "query block 2" in lib.rt_last_error().decode()
+    assert lib.rt_index_build(ctypes.byref(p), 256, 64, FAKE, FAKE, 16, None) == _lib.RT_EINVAL
+    stacked = np.stack([np.eye(4, dtype=np.uint8), hm])
+    p = _pat(kind=0, mask=FAKE, host_mask=stacked.ctypes.data, n_masks=2)
+    assert lib.rt_index_size(ctypes.byref(p), 256, 64, ctypes.byref(n)) == _lib.RT_EINVAL
+    assert "mask 1" in lib.rt_last_error().decode()
+    with pytest.raises(rt.RettentionError, match="keeps no key block"):
+        rt.index_size(256, 64, synth.PAT_EXPLICIT, host_mask=hm)
+
+
+def test_outputs_must_not_overlap_inputs(lib):
+    d = _dims()  # each bf16 tensor is 64 KiB, each fp32 statistic 2 KiB
+    b = _bsr()
+    part = K + 64  # overlaps K partially
+    # every call below is valid except for the planted overlap, so each must
+    # return EINVAL before any launch
+    for o in (Q, K, V, part):
+        assert lib.rt_attn_full(Q, K, V, d, 64, o, None, None, None) == _lib.RT_EINVAL
+        assert "overlaps" in lib.rt_last_error().decode()
+        assert lib.rt_attn_sparse(Q, K, V, d, ctypes.byref(b), o, None, None, None) == _lib.RT_EINVAL
+        assert lib.rt_attn_postmask(Q, K, V, d, ctypes.byref(b), o, None) == _lib.RT_EINVAL
+        assert lib.rt_attn_sparse_reshape(Q, K, V, d, ctypes.byref(b), S1, O2, 0.0, o, None, None,
+                                          None) == _lib.RT_EINVAL
+        assert lib.rt_attn_cache(Q, K, V, d, ctypes.byref(b), o, None, None, S1, O2, None) == _lib.RT_EINVAL
+    # the fused call's output against its residual and ratio
+    assert lib.rt_attn_sparse_reshape(Q, K, V, d, ctypes.byref(b), S1, O2, 0.0, O2, None, None,
+                                      None) == _lib.RT_EINVAL
+    assert lib.rt_attn_sparse_reshape(Q, K, V, d, ctypes.byref(b), O + 1024, O2, 0.0, O, None, None,
+                                      None) == _lib.RT_EINVAL
+    # statistics against the output, each other, and the fused call's inputs
+    assert lib.rt_attn_full(Q, K, V, d, 64, O, O + 64, None, None) == _lib.RT_EINVAL
+    assert lib.rt_attn_full(Q, K, V, d, 64, O, S1, S1 + 1024, None) == _lib.RT_EINVAL
+    assert lib.rt_attn_sparse_reshape(Q, K, V, d, ctypes.byref(b), S1, O2, 0.0, O, S1, None,
+                                      None) == _lib.RT_EINVAL
+    # caching step: resid against the inputs and o, rho against everything
+    assert lib.rt_attn_cache(Q, K, V, d, ctypes.byref(b), O, None, None, S1, K, None) == _lib.RT_EINVAL
+    assert lib.rt_attn_cache(Q, K, V, d, ctypes.byref(b), O, None, None, S1, O, None) == _lib.RT_EINVAL
+    assert lib.rt_attn_cache(Q, K, V, d, ctypes.byref(b), O, None, None, O2 + 256, O2, None) == _lib.RT_EINVAL
+    assert lib.rt_attn_cache(Q, K, V, d, ctypes.byref(b), O, S1, None, S1, O2, None) == _lib.RT_EINVAL
+    # element-wise calls: outputs against inputs
+    assert lib.rt_reshape_apply(Q, S1, K, 0.0, d, Q, None) == _lib.RT_EINVAL
+    assert lib.rt_reshape_apply(Q, S1, K, 0.0, d, K + 16, None) == _lib.RT_EINVAL
+    assert lib.rt_reshape_apply(Q, S1, K, 0.0, d, S1 - 16, None) == _lib.RT_EINVAL
+    assert lib.rt_cache_build(Q, S1, S2, K, S3, S4, d, S5, Q, None) == _lib.RT_EINVAL
+    assert lib.rt_cache_build(Q, S1, S2, K, S3, S4, d, S4, O, None) == _lib.RT_EINVAL
+    assert lib.rt_cache_build(Q, S1, S2, K, S3, S4, d, O + 16, O, None) == _lib.RT_EINVAL
+    assert "overlaps" in lib.rt_last_error().decode()

@@ -180,7 +180,12 @@ def test_malformed_csr_is_guarded(gpu):
     # row 0: indices out of range around a valid 0; row 1: empty; rows 2-3 overrun nnz
     row_ptr = np.array([0, 3, 3, 5, 9], dtype=np.int32)
     col_idx = np.array([-4, 0, 77, 2, 1], dtype=np.int32)
-    mask = rt.BlockMask.from_csr(row_ptr, col_idx, block)
+    # a host copy is checked and refused (Eq.5 needs a kept key in every row)
+    with pytest.raises(rt.RettentionError, match="keeps no key block|outside"):
+        rt.BlockMask.from_csr(row_ptr, col_idx, block)
+    # a device CSR the host never checked reaches the kernels, whose guards keep
+    # every access in bounds
+    mask = rt.BlockMask(torch.from_numpy(row_ptr).cuda(), torch.from_numpy(col_idx).cuda(), block, 4, 5)
     o, m, l = rt.attn_sparse(q, k, v, mask)
     torch.cuda.synchronize()
     O = to_np(o)[0, 0]

@@ -109,7 +109,13 @@ def test_cache_step_density_one_and_empty_rows(gpu):
     q, k, v = (to_dev(x) for x in s1)
     hm = np.eye(4, dtype=np.uint8)
     hm[2, :] = 0
-    mask = rt.build_index(T, block, synth.PAT_EXPLICIT, host_mask=hm)
+    # the host-side builders refuse such a mask (Eq.5 needs a kept key) ...
+    with pytest.raises(rt.RettentionError, match="keeps no key block"):
+        rt.build_index(T, block, synth.PAT_EXPLICIT, host_mask=hm)
+    # ... but a device CSR the host never checked still gets the caching step's
+    # defined answer for that row
+    rp_h, ci_h = ob.block_index_explicit(hm)
+    mask = rt.BlockMask(torch.from_numpy(rp_h).cuda(), torch.from_numpy(ci_h).cuda(), block, 4, int(rp_h[-1]))
     o, rho, resid, m, l = rt.attn_cache(q, k, v, mask)
     torch.cuda.synchronize()
     Q, K, V = (f64(x) for x in s1)
