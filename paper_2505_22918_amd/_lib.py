@@ -12,7 +12,9 @@ import os
 import re
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_PKG, "librettention.so")
+# RT_LIB_PATH selects another build of the same C ABI (the host-only sanitizer
+# build that the CPU tests drive); there is still no fallback when it is missing.
+LIB_PATH = os.environ.get("RT_LIB_PATH") or os.path.join(_PKG, "librettention.so")
 HEADER = os.path.join(os.path.dirname(_PKG), "include", "rettention.h")
 
 RT_OK, RT_EINVAL, RT_EUNSUPPORTED, RT_ECAPACITY, RT_EHIP = range(5)

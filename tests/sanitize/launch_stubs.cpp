@@ -1,0 +1,62 @@
+// Host-only stand-ins for the kernel launchers of csrc/kernels.h, so that the C
+// ABI (csrc/api.cpp) can be built with the host compiler under AddressSanitizer
+// and UndefinedBehaviorSanitizer and driven by the ABI tests without a GPU.
+// Each stand-in checks what the validation layer hands it and launches nothing;
+// a violated expectation aborts the process.
+#include <hip/hip_runtime_api.h>
+
+#include <cstdio>
+#include <cstdlib>
+
+#include "kernels.h"
+
+#define EXPECT(c)                                                                  \
+    do {                                                                           \
+        if (!(c)) {                                                                \
+            std::fprintf(stderr, "launch stub: expectation failed: %s\n", #c);    \
+            std::abort();                                                          \
+        }                                                                          \
+    } while (0)
+
+extern "C" const char* hipGetErrorString(hipError_t) { return "hip (stubbed)"; }
+
+namespace rt {
+
+hipError_t launch_attention(const AttnArgs& a, int D, int block, AttnMode mode, hipStream_t) {
+    EXPECT(D == 64 || D == 72);
+    EXPECT(block == 32 || block == 64);
+    EXPECT(a.q && a.k && a.v && a.o);
+    EXPECT(a.T > 0 && a.n_blk == (a.T + block - 1) / block);
+    EXPECT(a.n_items > 0 && a.n_items % a.n_blk == 0);
+    EXPECT(8LL * a.per_xcd >= a.n_items && 8LL * (a.per_xcd - 1) < a.n_items);
+    EXPECT((long long)a.T * D * 2 <= (1LL << 30));
+    if (!a.dense) {
+        EXPECT(a.row_ptr && a.col_idx && a.nnz > 0 && a.n_masks >= 1);
+    }
+    if (mode == kAttnReshape) EXPECT(a.rho && a.resid);
+    if (mode == kAttnCache && !a.postmask) EXPECT(a.rho_out && a.resid_out);
+    return hipSuccess;
+}
+
+hipError_t launch_cache_build(const uint16_t* o_full, const float* m_full, const float* l_full,
+                              const uint16_t* o_sparse, const float* m_sparse, const float* l_sparse,
+                              int64_t rows, int D, float* rho, uint16_t* resid, hipStream_t) {
+    EXPECT(o_full && m_full && l_full && o_sparse && m_sparse && l_sparse && rho && resid);
+    EXPECT(rows > 0 && (D == 64 || D == 72));
+    return hipSuccess;
+}
+
+hipError_t launch_reshape_apply(const uint16_t* o_sparse, const float* rho, const uint16_t* resid,
+                                float, int64_t rows, int D, uint16_t* o, hipStream_t) {
+    EXPECT(o_sparse && rho && resid && o && rows > 0 && (D == 64 || D == 72));
+    return hipSuccess;
+}
+
+hipError_t launch_index_build(const IndexArgs& a, hipStream_t) {
+    EXPECT(a.row_ptr && a.col_idx && a.T > 0 && a.n_blk == (a.T + a.block - 1) / a.block);
+    EXPECT(a.n_blk <= 4096 && a.n_masks >= 1 && a.capacity >= 0);
+    if (a.kind == 0) EXPECT(a.mask);
+    return hipSuccess;
+}
+
+}  // namespace rt
