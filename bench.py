@@ -164,6 +164,54 @@ def cpu_baseline(wl, s2, rp, ci, rho, resid, budget_s=12.0):
     return t_total, done, len(heads), blas_threads
 
 
+def other_workload(name, steps, warmup, dev):
+    """The fused call on another workload, timed the same way as the main one
+    (K back-to-back calls between HIP events on the launch stream), with its
+    dense attention beside it.  Inputs are made, used and freed here."""
+    import torch
+
+    import paper_2505_22918_amd as rt
+    from paper_2505_22918_amd import synth
+
+    wl = synth.WORKLOADS[name]
+    to_dev = lambda b: torch.from_numpy(np.ascontiguousarray(b).view(np.int16)).to(dev).view(torch.bfloat16)
+    kw = {k: v for k, v in wl.pattern_kwargs().items() if k != "kind"}
+    if wl.kind == synth.PAT_EXPLICIT:
+        mask = rt.build_index(wl.T, wl.block, wl.kind, device=dev,
+                              host_mask=synth.explicit_block_mask(wl.n_blk, wl.seed))
+    else:
+        mask = rt.build_index(wl.T, wl.block, wl.kind, device=dev, **kw)
+    rp, ci = mask.row_ptr.cpu().numpy(), mask.col_idx.cpu().numpy()
+    flops = kept_flops(wl, rp, ci)
+    q1, k1, v1 = (to_dev(x) for x in synth.make_qkv(wl, 1))
+    q2, k2, v2 = (to_dev(x) for x in synth.make_qkv(wl, 2))
+    of, rho, resid = rt.attn_cache(q1, k1, v1, mask, stats=False)
+    out = torch.empty_like(q2)
+    stream = torch.cuda.current_stream()
+    fused = lambda: rt.attn_sparse_reshape(q2, k2, v2, mask, rho, resid, 0.0, out=out)
+    for _ in range(warmup):
+        fused()
+    ms = time_calls(fused, steps, stream)
+    t_dense = time_calls(lambda: rt.attn_full(q2, k2, v2, block=wl.block, stats=False, out=of), 3, stream)
+    tflops = flops / (ms * 1e-3) / 1e12
+    gbs = fused_bytes(wl) / (ms * 1e-3) / 1e9
+    rec = {
+        "us_per_call": ms * 1e3,
+        "kept_tflops": tflops,
+        "mfma_frac": tflops / PEAK_BF16_TFLOPS,
+        "hbm_gbs": gbs,
+        "hbm_frac": gbs / PEAK_HBM_GBS,
+        "dense_us": t_dense * 1e3,
+        "dense_tflops": 4.0 * wl.B * wl.H * wl.T * wl.T * wl.D / (t_dense * 1e-3) / 1e12,
+        "speedup_vs_dense": t_dense / ms,
+        "config": {"B": wl.B, "H": wl.H, "T": wl.T, "D": wl.D, "block": wl.block, "nnz_blocks": int(mask.nnz),
+                   "kept_gflop": flops / 1e9, "algorithmic_mb": fused_bytes(wl) / 1e6},
+    }
+    del q1, k1, v1, q2, k2, v2, of, rho, resid, out, mask
+    torch.cuda.empty_cache()
+    return rec
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -180,6 +228,9 @@ def main():
                          "kernel runs with less switching, which shows how the clock depends on the data")
     ap.add_argument("--copy-mb", type=int, default=0,
                     help="also run K plain device copies of this many MiB (HBM counter calibration)")
+    ap.add_argument("--other-workloads", default="all",
+                    help="'all' (default), 'none' or a comma list: the fused call on the other workloads, "
+                         "reported under \"workloads\"")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -346,6 +397,24 @@ def main():
         cpu["dense_ms_per_call_extrapolated"] = t_dense_cpu * wl.B * wl.H * 1e3
         log(f"cpu oracle: {cpu}")
 
+    others = {}
+    names = [n for n in synth.WORKLOADS if n != wl.name]
+    if args.other_workloads == "none":
+        names = []
+    elif args.other_workloads != "all":
+        names = [n for n in args.other_workloads.split(",") if n and n != wl.name]
+    for name in names:
+        others[name] = other_workload(name, args.steps, args.warmup, dev)
+        log(f"workload {name}: {others[name]['us_per_call']:.1f} us/call, {others[name]['kept_tflops']:.1f} "
+            f"TFLOP/s ({others[name]['mfma_frac']:.1%}), {others[name]['hbm_gbs']:.0f} GB/s")
+    workloads = {wl.name: {
+        "us_per_call": ms_call * 1e3, "kept_tflops": tflops, "mfma_frac": tflops / PEAK_BF16_TFLOPS,
+        "hbm_gbs": gbs, "hbm_frac": gbs / PEAK_HBM_GBS,
+        "dense_us": path["attn_full_ms"] * 1e3 if path else None,
+        "speedup_vs_dense": path.get("speedup_vs_dense") if path else None,
+    }}
+    workloads.update(others)
+
     bound = "hbm" if ai < ridge else "mfma"
     traffic = measured_traffic(wl.name)
     exec_flops = executed_flops(wl, mask.nnz)
@@ -392,6 +461,7 @@ def main():
         "roofline": roof,
         "cpu_baseline": cpu,
         "path": path,
+        "workloads": workloads,
     }
     print(json.dumps(rec), flush=True)
 
