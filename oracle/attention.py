@@ -21,6 +21,9 @@ sparse_attention  Eq.5      output, m_s, l_s over a block CSR mask
 rho               Eq.8      ratio of sparse to full denominators
 residual          Eq.10     R = FullAttention - rho * SparseAttention
 reshape           Eq.9 + ramp (Sec.4.2) + residual: min(1, rho + delta) O_s + R
+residual_no_ratio the same cache without the statistical reshape: Eq.10 with the
+                  ratio fixed at one, R' = FullAttention - SparseAttention
+add_residual      that ablation's later output, O_s(t) + R' (no Eq.9 scaling)
 brute_force       Eq.2-5, 7, 8, 10 and the App. A.3 decomposition written as
                   literal T x T matrices (tiny inputs only)
 
@@ -32,6 +35,10 @@ Readings of the paper taken here, where its text leaves the choice open:
   * R is added unscaled (Sec.4.2, "Residual Caching").
   * a key block past the end of the sequence contributes no keys (the mask
     covers only tokens 0 .. T-1).
+  * the paper compares against sliding-window attention with caching at the
+    same full-attention steps (Sec.5, App. A.4) but prints no formula for that
+    scheme's cache; the ablation here keeps Re-ttention's residual caching and
+    drops the reshape, i.e. Eq.10 with rho = 1.
 """
 
 from __future__ import annotations
@@ -48,6 +55,8 @@ __all__ = [
     "rho",
     "residual",
     "reshape",
+    "residual_no_ratio",
+    "add_residual",
     "brute_force",
 ]
 
@@ -195,6 +204,19 @@ def reshape(o_sparse, rho_, resid, rho_delta=0.0):
     return r[..., None] * _f64(o_sparse) + _f64(resid)
 
 
+def residual_no_ratio(o_full, o_sparse):
+    """Eq.10 with the ratio fixed at one: R' = FullAttention - SparseAttention at
+    the caching step (the cache of the ablation without the statistical
+    reshape)."""
+    return _f64(o_full) - _f64(o_sparse)
+
+
+def add_residual(o_sparse, resid):
+    """The ablation's output at a later step: O_s(t) + R', the sparse output
+    unscaled (no Eq.9) plus the cached gap."""
+    return _f64(o_sparse) + _f64(resid)
+
+
 def brute_force(q, k, v, mask, rho_delta=0.0):
     """Literal matrix forms for one head: q, k, v [T, d]; mask M [T, T] in {0, 1}.
 
@@ -209,6 +231,7 @@ def brute_force(q, k, v, mask, rho_delta=0.0):
       resid     Eq.10: A V - rho * A_sparse V
       resid_out App. A.3: A_{not in S} V (independent of Eq.10's subtraction)
       reshaped  (min(1, rho + delta) * A_sparse) V + resid
+      resid_no_ratio  Eq.10 with rho = 1: A V - A_sparse V
     """
     q = _f64(q)
     k = _f64(k)
@@ -232,6 +255,7 @@ def brute_force(q, k, v, mask, rho_delta=0.0):
     o_full = a @ v
     o_sparse = a_sparse @ v
     resid = o_full - rho_[:, None] * o_sparse
+    resid_no_ratio = o_full - o_sparse
     r = np.minimum(1.0, rho_ + rho_delta)
     reshaped = (r[:, None] * a_sparse) @ v + resid
     return {
@@ -248,6 +272,7 @@ def brute_force(q, k, v, mask, rho_delta=0.0):
         "resid": resid,
         "resid_out": a_out @ v,
         "reshaped": reshaped,
+        "resid_no_ratio": resid_no_ratio,
         "full_den": full_den,
         "sparse_den": sparse_den,
     }

@@ -36,10 +36,12 @@ def caching_steps(n_steps, full_steps, period):
     return out
 
 
-def run(steps_qkv, row_ptr, col_idx, block, full_steps, period, lam):
+def run(steps_qkv, row_ptr, col_idx, block, full_steps, period, lam, ratio=True):
     """Attention outputs of a denoising run: steps_qkv is a list of (q, k, v)
     arrays [B, H, T, d] per step.  Returns (outputs, ratios) where ratios[t] is
-    the ramped ratio applied at step t (None at caching steps)."""
+    the ramped ratio applied at step t (None at caching steps).  ratio=False
+    runs the ablation without the statistical reshape: the cache holds
+    R' = O_full - O_sparse and later steps output O_sparse + R' (ratios None)."""
     full = caching_steps(len(steps_qkv), full_steps, period)
     outs, ratios = [], []
     rho_c = resid_c = None
@@ -49,13 +51,17 @@ def run(steps_qkv, row_ptr, col_idx, block, full_steps, period, lam):
             o_f, m_f, l_f = oa.full_attention(q, k, v)
             o_s, m_s, l_s = oa.sparse_attention(q, k, v, row_ptr, col_idx, block)
             rho_c = oa.rho(m_s, l_s, m_f, l_f)
-            resid_c = oa.residual(o_f, o_s, rho_c)
+            resid_c = oa.residual(o_f, o_s, rho_c) if ratio else oa.residual_no_ratio(o_f, o_s)
             c = t
             outs.append(o_f)
             ratios.append(None)
         else:
             o_s, _, _ = oa.sparse_attention(q, k, v, row_ptr, col_idx, block)
-            delta = lam * (t - c)
-            outs.append(oa.reshape(o_s, rho_c, resid_c, delta))
-            ratios.append(np.minimum(1.0, rho_c + delta))
+            if ratio:
+                delta = lam * (t - c)
+                outs.append(oa.reshape(o_s, rho_c, resid_c, delta))
+                ratios.append(np.minimum(1.0, rho_c + delta))
+            else:
+                outs.append(oa.add_residual(o_s, resid_c))
+                ratios.append(None)
     return outs, ratios

@@ -262,3 +262,55 @@ def test_empty_kept_set_is_rejected():
     ci = np.array([1], dtype=np.int32)
     with pytest.raises(ValueError):
         oa.sparse_attention(q, k, v, rp, ci, 16)
+
+
+# ---- the ablation without the statistical reshape (Eq.10 with rho = 1) -----
+
+def test_no_ratio_residual_is_masked_attention_minus_the_missing_mass():
+    # App. A.3 splits O_full = rho O_s + A_{not in S} V, so the ratio-free cache
+    # R' = O_full - O_s equals A_{not in S} V - (1 - rho) O_s; both sides built
+    # independently from the literal matrices (scipy softmax, masked sums)
+    q, k, v, rp, ci, bs, M = _brute_case(seed=19)
+    of, mf, lf = oa.full_attention(q, k, v)
+    os_, ms, ls = oa.sparse_attention(q, k, v, rp, ci, bs)
+    Rn = oa.residual_no_ratio(of, os_)[0, 0]
+    a_pre = q[0, 0] @ k[0, 0].T / np.sqrt(q.shape[-1])
+    a = scipy.special.softmax(a_pre, axis=1)
+    rho_lit = (a * M).sum(axis=1)  # Eq.8 as the kept share of each softmax row
+    a_sp = np.where(M > 0, np.exp(a_pre), 0.0)
+    o_s_lit = (a_sp / a_sp.sum(axis=1, keepdims=True)) @ v[0, 0]
+    rhs = (a * (1 - M)) @ v[0, 0] - (1.0 - rho_lit)[:, None] * o_s_lit
+    np.testing.assert_allclose(Rn, rhs, rtol=1e-10, atol=1e-12)
+    bf = oa.brute_force(q[0, 0], k[0, 0], v[0, 0], M)
+    np.testing.assert_allclose(bf["resid_no_ratio"], rhs, rtol=1e-10, atol=1e-12)
+
+
+def test_no_ratio_ablation_reconstructs_full_attention_at_caching_step():
+    q, k, v, rp, ci, bs, M = _brute_case(seed=21)
+    of, _, _ = oa.full_attention(q, k, v)
+    os_, _, _ = oa.sparse_attention(q, k, v, rp, ci, bs)
+    out = oa.add_residual(os_, oa.residual_no_ratio(of, os_))
+    np.testing.assert_allclose(out, of, rtol=1e-12, atol=1e-14)
+
+
+def test_no_ratio_residual_closed_forms():
+    # density one: nothing is missing, the cache is zero
+    q, k, v, *_ = _tiny_case(seed=23, T=48, d=8, bs=16)
+    rp, ci = _csr_all(3)
+    of, _, _ = oa.full_attention(q, k, v)
+    os_, _, _ = oa.sparse_attention(q, k, v, rp, ci, 16)
+    np.testing.assert_allclose(oa.residual_no_ratio(of, os_), 0.0, atol=1e-13)
+    # uniform scores (Q = 0): R' = mean of all V - mean of the kept V
+    T, d, bs = 40, 8, 8
+    q = np.zeros((1, 1, T, d))
+    k = _rand((1, 1, T, d), 1)
+    v = _rand((1, 1, T, d), 2)
+    mask = synth.explicit_block_mask(ob.n_blocks(T, bs), seed=4, extra=2)
+    rp, ci = ob.block_index_explicit(mask)
+    of, _, _ = oa.full_attention(q, k, v)
+    os_, _, _ = oa.sparse_attention(q, k, v, rp, ci, bs)
+    Rn = oa.residual_no_ratio(of, os_)
+    for i in range(T):
+        S = oa.kept_tokens(rp, ci, i // bs, bs, T)
+        np.testing.assert_allclose(Rn[0, 0, i], v[0, 0].mean(axis=0) - v[0, 0, S].mean(axis=0), rtol=1e-12,
+                                   atol=1e-14)

@@ -34,6 +34,8 @@ def _pins_hold(mod):
         r = mod.rho(ms, ls, mf, lf)
         R = mod.residual(of, os_, r)
         out = mod.reshape(os_, r, R, 0.0)
+        Rn = mod.residual_no_ratio(of, os_)
+        out_n = mod.add_residual(os_, Rn)
         M = ob.token_mask(rp, ci, bs, T).astype(bool)
         for h in range(2):
             a_pre = q[0, h] @ k[0, h].T / np.sqrt(q.shape[-1])
@@ -44,7 +46,13 @@ def _pins_hold(mod):
                   and np.allclose(os_[0, h], a_s @ v[0, h], rtol=1e-10, atol=1e-12)
                   and np.allclose(r[0, h], np.where(M, a, 0).sum(axis=1), rtol=1e-10)
                   and np.allclose(R[0, h], np.where(M, 0, a) @ v[0, h], rtol=1e-9, atol=1e-12)
-                  and np.allclose(out[0, h], a @ v[0, h], rtol=1e-9, atol=1e-12))
+                  and np.allclose(out[0, h], a @ v[0, h], rtol=1e-9, atol=1e-12)
+                  # the ratio-free ablation (Eq.10 with rho = 1), against the
+                  # App. A.3 split O_full = rho O_s + A_{not in S} V
+                  and np.allclose(Rn[0, h], np.where(M, 0, a) @ v[0, h]
+                                  - (1.0 - np.where(M, a, 0).sum(axis=1))[:, None] * (a_s @ v[0, h]),
+                                  rtol=1e-9, atol=1e-12)
+                  and np.allclose(out_n[0, h], a @ v[0, h], rtol=1e-9, atol=1e-12))
             if not ok:
                 return False
         # ramp clamp
@@ -56,7 +64,8 @@ def _pins_hold(mod):
 
 class _Mod:
     def __init__(self, **over):
-        for name in ("full_attention", "sparse_attention", "rho", "residual", "reshape"):
+        for name in ("full_attention", "sparse_attention", "rho", "residual", "reshape", "residual_no_ratio",
+                     "add_residual"):
             setattr(self, name, over.get(name, getattr(oa, name)))
 
 
@@ -107,6 +116,14 @@ def _mut_sparse_full_denominator(q, k, v, rp, ci, bs):
     return os_ * r[..., None], ms, ls
 
 
+def _mut_no_ratio_sign(of, os_):
+    return np.asarray(os_) - np.asarray(of)
+
+
+def _mut_no_ratio_scaled_output(os_, R):
+    return 0.5 * (np.asarray(os_) + np.asarray(R))
+
+
 @pytest.mark.parametrize("over", [
     dict(rho=_mut_rho_drop_exp),
     dict(residual=_mut_residual_sign),
@@ -116,8 +133,12 @@ def _mut_sparse_full_denominator(q, k, v, rp, ci, bs):
     dict(full_attention=_mut_full_transposed),
     dict(sparse_attention=_mut_sparse_phantom),
     dict(sparse_attention=_mut_sparse_full_denominator),
+    dict(residual_no_ratio=_mut_no_ratio_sign),
+    dict(add_residual=_mut_no_ratio_scaled_output),
+    dict(residual_no_ratio=lambda of, os_: np.asarray(of) - 0.9 * np.asarray(os_)),
 ], ids=["rho-drop-exp", "residual-sign", "no-clamp", "resid-scaled", "scale-d",
-        "transposed", "phantom-keys", "post-softmax"])
+        "transposed", "phantom-keys", "post-softmax", "no-ratio-sign", "no-ratio-output-scaled",
+        "no-ratio-keeps-a-ratio"])
 def test_mutant_is_caught(over):
     assert not _pins_hold(_Mod(**over))
 

@@ -76,3 +76,17 @@ def test_evolve_is_seeded_and_small():
     assert not all(np.array_equal(x, y) for x, y in zip(a, c))
     dq = synth.bf16_bits_to_f32(a[0]) - synth.bf16_bits_to_f32(s1[0])
     assert 0.04 < float(dq.std()) < 0.06
+
+
+def test_no_ratio_ablation_with_still_inputs_returns_full_attention():
+    # without drift every later step sees the caching step's inputs, so O_s(t)
+    # equals O_s(c) and O_s + (O_full - O_s) is full attention at every step
+    rng = np.random.default_rng(31)
+    q, k, v = (rng.standard_normal((1, 2, 40, 8)) for _ in range(3))
+    mask = synth.explicit_block_mask(5, seed=2, extra=1)
+    rp, ci = ob.block_index_explicit(mask)
+    outs, ratios = osch.run([(q, k, v)] * 7, rp, ci, 8, 2, 3, 0.0, ratio=False)
+    of, _, _ = oa.full_attention(q, k, v)
+    for t, o in enumerate(outs):
+        np.testing.assert_allclose(o, of, rtol=1e-12, atol=1e-13)
+        assert ratios[t] is None
