@@ -173,7 +173,11 @@ rt_status rt_attn_sparse(const void* q, const void* k, const void* v, rt_dims di
  * must not alias q, k, v or each other); rho: device fp32 [B,H,T] (written);
  * row_max / row_sum: device fp32 [B,H,T], the full-attention statistics, or
  * NULL.  Rows whose query block keeps every key block get rho = 1, R = 0; a
- * query block with no kept block gets rho = 0, R = O_full. */
+ * query block with no kept block gets rho = 0, R = O_full.
+ * rho may be NULL: the cache of the ablation without the statistical reshape
+ * (Eq.10 with the ratio fixed at one, the window-attention-plus-caching scheme
+ * the paper compares against in Sec.5 and App. A.4) is then written instead,
+ * resid = O_full - O_S (O_full where the query block keeps no block). */
 rt_status rt_attn_cache(const void* q, const void* k, const void* v, rt_dims dims, const rt_bsr* mask,
                         void* o, float* row_max, float* row_sum, float* rho, void* resid, void* stream);
 
@@ -191,7 +195,8 @@ rt_status rt_attn_postmask(const void* q, const void* k, const void* v, rt_dims 
  *   R   = O_full - rho * O_sparse                           (Eq.10)
  * o_full, o_sparse: device bf16 [B,H,T,D]; m_*, l_*: device fp32 [B,H,T];
  * rho: device fp32 [B,H,T] (written); resid: device bf16 [B,H,T,D] (written,
- * rounded to nearest even). */
+ * rounded to nearest even).  With rho NULL (the ablation without the reshape)
+ * R = O_full - O_sparse is written and m_*, l_* are not read (may be NULL). */
 rt_status rt_cache_build(const void* o_full, const float* m_full, const float* l_full,
                          const void* o_sparse, const float* m_sparse, const float* l_sparse,
                          rt_dims dims, float* rho, void* resid, void* stream);
@@ -202,7 +207,10 @@ rt_status rt_cache_build(const void* o_full, const float* m_full, const float* l
  * rho_delta = lambda * (t - c) is the ramp accumulated since the caching step
  * c (0 for no ramp).  rho: device fp32 [B,H,T]; resid: device bf16 [B,H,T,D];
  * o: device bf16 [B,H,T,D] (written); row_max / row_sum: device fp32 [B,H,T],
- * the sparse statistics of this step, or NULL to skip writing them. */
+ * the sparse statistics of this step, or NULL to skip writing them.
+ * rho may be NULL: the ablation without the statistical reshape then computes
+ * O = SparseAttention(Q,K,V) + R (no Eq.9 scaling; rho_delta is ignored), with R
+ * the ratio-free cache of rt_attn_cache / rt_cache_build. */
 rt_status rt_attn_sparse_reshape(const void* q, const void* k, const void* v, rt_dims dims,
                                  const rt_bsr* mask, const float* rho, const void* resid,
                                  float rho_delta, void* o, float* row_max, float* row_sum,
@@ -212,7 +220,8 @@ rt_status rt_attn_sparse_reshape(const void* q, const void* k, const void* v, rt
  * Eq.9 scales the sparse softmax output by the cached ratio, ramped by
  * rho_delta as in Sec.4.2 and clamped to 1, and Eq.10 adds the cached residual:
  *   O = min(1, rho + rho_delta) * o_sparse + R
- * o_sparse, resid, o: device bf16 [B,H,T,D]; rho: device fp32 [B,H,T]. */
+ * o_sparse, resid, o: device bf16 [B,H,T,D]; rho: device fp32 [B,H,T], or NULL
+ * for the ablation without the reshape (O = o_sparse + R). */
 rt_status rt_reshape_apply(const void* o_sparse, const float* rho, const void* resid,
                            float rho_delta, rt_dims dims, void* o, void* stream);
 

@@ -252,20 +252,22 @@ def attn_sparse(q, k, v, mask: BlockMask, stats=True, out=None):
     return (o, m, l) if stats else o
 
 
-def attn_cache(q, k, v, mask: BlockMask, stats=True, out=None):
+def attn_cache(q, k, v, mask: BlockMask, stats=True, out=None, ratio=True):
     """One-pass caching step (App. A.3): full attention over every key block with
-    the keys split by the mask.  Returns (O_full, rho, R[, m_full, l_full])."""
+    the keys split by the mask.  Returns (O_full, rho, R[, m_full, l_full]).
+    ratio=False caches the ablation without the statistical reshape (rho is
+    None, R = O_full - O_sparse: Eq.10 with the ratio fixed at one)."""
     torch = _torch()
     lib = _lib.load()
     dims = _check_qkv(q, k, v)
     _mask_on(mask, q.device)
     o = _out(out, q)
-    rho = torch.empty(q.shape[:3], dtype=torch.float32, device=q.device)
+    rho = torch.empty(q.shape[:3], dtype=torch.float32, device=q.device) if ratio else None
     resid = torch.empty_like(q)
     m = l = None
     if stats:
-        m = torch.empty_like(rho)
-        l = torch.empty_like(rho)
+        m = torch.empty(q.shape[:3], dtype=torch.float32, device=q.device)
+        l = torch.empty_like(m)
     bsr = mask.c_struct()
     _lib.check("rt_attn_cache", lib.rt_attn_cache(_ptr(q), _ptr(k), _ptr(v), dims, ctypes.byref(bsr), _ptr(o),
                                                   _ptr(m), _ptr(l), _ptr(rho), _ptr(resid), _stream(q)))
@@ -285,8 +287,10 @@ def attn_postmask(q, k, v, mask: BlockMask, out=None):
     return o
 
 
-def cache_build(o_full, m_full, l_full, o_sparse, m_sparse, l_sparse):
-    """rho (Eq.8) and residual R (Eq.10) at a caching step."""
+def cache_build(o_full, m_full, l_full, o_sparse, m_sparse, l_sparse, ratio=True):
+    """rho (Eq.8) and residual R (Eq.10) at a caching step.  ratio=False: the
+    ablation without the reshape, rho None and R = O_full - O_sparse (the
+    statistics are not read and may be None)."""
     torch = _torch()
     lib = _lib.load()
     _on_device(o_full, "o_full", None)
@@ -296,9 +300,12 @@ def cache_build(o_full, m_full, l_full, o_sparse, m_sparse, l_sparse):
     B, H, T, D = o_full.shape
     _bf16(o_full, o_full.shape, "o_full", dev)
     _bf16(o_sparse, o_full.shape, "o_sparse", dev)
-    for name, t in (("m_full", m_full), ("l_full", l_full), ("m_sparse", m_sparse), ("l_sparse", l_sparse)):
-        _stat(t, (B, H, T), name, dev)
-    rho = torch.empty((B, H, T), dtype=torch.float32, device=o_full.device)
+    if ratio:
+        for name, t in (("m_full", m_full), ("l_full", l_full), ("m_sparse", m_sparse), ("l_sparse", l_sparse)):
+            _stat(t, (B, H, T), name, dev)
+    else:
+        m_full = l_full = m_sparse = l_sparse = None
+    rho = torch.empty((B, H, T), dtype=torch.float32, device=o_full.device) if ratio else None
     resid = torch.empty_like(o_full)
     _lib.check("rt_cache_build", lib.rt_cache_build(_ptr(o_full), _ptr(m_full), _ptr(l_full), _ptr(o_sparse),
                                                     _ptr(m_sparse), _ptr(l_sparse), _lib.RtDims(B, H, T, D),
@@ -307,12 +314,14 @@ def cache_build(o_full, m_full, l_full, o_sparse, m_sparse, l_sparse):
 
 
 def attn_sparse_reshape(q, k, v, mask: BlockMask, rho, resid, rho_delta=0.0, stats=False, out=None):
-    """Fused Eq.5 + Eq.9 (ramped) + Eq.10: min(1, rho + delta) * SparseAttn + R."""
+    """Fused Eq.5 + Eq.9 (ramped) + Eq.10: min(1, rho + delta) * SparseAttn + R.
+    rho=None: the ablation without the reshape, SparseAttn + R."""
     torch = _torch()
     lib = _lib.load()
     dims = _check_qkv(q, k, v)
     _mask_on(mask, q.device)
-    _stat(rho, q.shape[:3], "rho", q.device)
+    if rho is not None:
+        _stat(rho, q.shape[:3], "rho", q.device)
     _bf16(resid, q.shape, "resid", q.device)
     o = _out(out, q)
     m = l = None
@@ -327,7 +336,8 @@ def attn_sparse_reshape(q, k, v, mask: BlockMask, rho, resid, rho_delta=0.0, sta
 
 
 def reshape_apply(o_sparse, rho, resid, rho_delta=0.0, out=None):
-    """Unfused Eq.9 + Eq.10 on a sparse output: min(1, rho + delta) * o_sparse + R."""
+    """Unfused Eq.9 + Eq.10 on a sparse output: min(1, rho + delta) * o_sparse + R
+    (rho=None: o_sparse + R, the ablation without the reshape)."""
     torch = _torch()
     lib = _lib.load()
     _on_device(o_sparse, "o_sparse", None)
@@ -337,7 +347,8 @@ def reshape_apply(o_sparse, rho, resid, rho_delta=0.0, out=None):
     B, H, T, D = o_sparse.shape
     _bf16(o_sparse, o_sparse.shape, "o_sparse", dev)
     _bf16(resid, o_sparse.shape, "resid", dev)
-    _stat(rho, (B, H, T), "rho", dev)
+    if rho is not None:
+        _stat(rho, (B, H, T), "rho", dev)
     o = _out(out, o_sparse)
     _lib.check("rt_reshape_apply", lib.rt_reshape_apply(_ptr(o_sparse), _ptr(rho), _ptr(resid), float(rho_delta),
                                                         _lib.RtDims(B, H, T, D), _ptr(o), _stream(o_sparse)))
@@ -353,11 +364,14 @@ class StatCache:
     ramped by ``lam`` per step (Sec.4.2), i.e. rho_delta = lam * (t - c).
     """
 
-    def __init__(self, mask: BlockMask, full_steps=5, period=5, lam=0.0):
+    def __init__(self, mask: BlockMask, full_steps=5, period=5, lam=0.0, ratio=True):
         self.mask = mask
         self.full_steps = int(full_steps)
         self.period = int(period)
         self.lam = float(lam)
+        # ratio=False: the ablation without the statistical reshape (cache
+        # R = O_full - O_sparse, later steps SparseAttn + R)
+        self.ratio = bool(ratio)
         self.rho = None
         self.resid = None
         self.cached_at = None
@@ -372,8 +386,8 @@ class StatCache:
     def attend(self, q, k, v, t):
         """Attention output at denoising step t (full at caching steps, where the
         one-pass caching kernel also refreshes rho and R)."""
-        if self.is_caching_step(t) or self.rho is None:
-            o_f, self.rho, self.resid = attn_cache(q, k, v, self.mask, stats=False)
+        if self.is_caching_step(t) or self.resid is None:
+            o_f, self.rho, self.resid = attn_cache(q, k, v, self.mask, stats=False, ratio=self.ratio)
             self.cached_at = t
             return o_f
         delta = self.lam * (t - self.cached_at)

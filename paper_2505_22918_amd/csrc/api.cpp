@@ -385,15 +385,16 @@ rt_status rt_attn_cache(const void* q, const void* k, const void* v, rt_dims dim
     RT_TRY(check_bsr(mask, dims));
     if (empty) return ok();
     RT_TRY(check_qkv(q, k, v, o));
-    RT_TRY(check_stat(rho, "rho"));
+    if (rho) RT_TRY(check_stat(rho, "rho"));
     RT_TRY(check_tensor(resid, "resid"));
     if (row_max) RT_TRY(check_stat(row_max, "row_max"));
     if (row_sum) RT_TRY(check_stat(row_sum, "row_sum"));
     const int64_t nt = tensor_bytes(dims, 2), ns = tensor_bytes(dims, 4) / dims.D;
     RT_TRY(check_no_overlap(o, nt, "o", {{q, nt}, {k, nt}, {v, nt}, {resid, nt}}, "q, k, v or resid"));
     RT_TRY(check_no_overlap(resid, nt, "resid", {{q, nt}, {k, nt}, {v, nt}}, "q, k or v"));
-    RT_TRY(check_no_overlap(rho, ns, "rho", {{q, nt}, {k, nt}, {v, nt}, {o, nt}, {resid, nt}},
-                            "q, k, v, o or resid"));
+    if (rho)
+        RT_TRY(check_no_overlap(rho, ns, "rho", {{q, nt}, {k, nt}, {v, nt}, {o, nt}, {resid, nt}},
+                                "q, k, v, o or resid"));
     RT_TRY(check_stats_overlap(dims, row_max, row_sum, o, {{resid, nt}, {rho, ns}}));
     RT_TRY(check_items(dims, mask->block));
     rt::AttnArgs a = base_args(q, k, v, dims, mask->block, o, row_max, row_sum);
@@ -430,20 +431,25 @@ rt_status rt_cache_build(const void* o_full, const float* m_full, const float* l
     RT_TRY(check_tensor(o_full, "o_full"));
     RT_TRY(check_tensor(o_sparse, "o_sparse"));
     RT_TRY(check_tensor(resid, "resid"));
-    RT_TRY(check_stat(m_full, "m_full"));
-    RT_TRY(check_stat(l_full, "l_full"));
-    RT_TRY(check_stat(m_sparse, "m_sparse"));
-    RT_TRY(check_stat(l_sparse, "l_sparse"));
-    RT_TRY(check_stat(rho, "rho"));
+    if (rho) {  // without a ratio the statistics are not read
+        RT_TRY(check_stat(m_full, "m_full"));
+        RT_TRY(check_stat(l_full, "l_full"));
+        RT_TRY(check_stat(m_sparse, "m_sparse"));
+        RT_TRY(check_stat(l_sparse, "l_sparse"));
+        RT_TRY(check_stat(rho, "rho"));
+    }
     {
         const int64_t nt = tensor_bytes(dims, 2), ns = tensor_bytes(dims, 4) / dims.D;
         const std::initializer_list<std::pair<const void*, int64_t>> ins = {
             {o_full, nt}, {o_sparse, nt}, {m_full, ns}, {l_full, ns}, {m_sparse, ns}, {l_sparse, ns}};
         RT_TRY(check_no_overlap(resid, nt, "resid", ins, "an input"));
-        RT_TRY(check_no_overlap(rho, ns, "rho", ins, "an input"));
-        RT_TRY(check_no_overlap(rho, ns, "rho", {{resid, nt}}, "resid"));
+        if (rho) {
+            RT_TRY(check_no_overlap(rho, ns, "rho", ins, "an input"));
+            RT_TRY(check_no_overlap(rho, ns, "rho", {{resid, nt}}, "resid"));
+        }
     }
     const int64_t rows = (int64_t)dims.B * dims.H * dims.T;
+    if (!rho) m_full = l_full = m_sparse = l_sparse = nullptr;
     return hip_status(rt::launch_cache_build(static_cast<const uint16_t*>(o_full), m_full, l_full,
                                              static_cast<const uint16_t*>(o_sparse), m_sparse, l_sparse, rows,
                                              dims.D, rho, static_cast<uint16_t*>(resid),
@@ -460,7 +466,7 @@ rt_status rt_attn_sparse_reshape(const void* q, const void* k, const void* v, rt
     if (!std::isfinite(rho_delta)) return fail(RT_EINVAL, "rho_delta is not finite");
     if (empty) return ok();
     RT_TRY(check_qkv(q, k, v, o));
-    RT_TRY(check_stat(rho, "rho"));
+    if (rho) RT_TRY(check_stat(rho, "rho"));
     RT_TRY(check_tensor(resid, "resid"));
     if (row_max) RT_TRY(check_stat(row_max, "row_max"));
     if (row_sum) RT_TRY(check_stat(row_sum, "row_sum"));
@@ -487,7 +493,7 @@ rt_status rt_reshape_apply(const void* o_sparse, const float* rho, const void* r
     RT_TRY(check_tensor(o_sparse, "o_sparse"));
     RT_TRY(check_tensor(resid, "resid"));
     RT_TRY(check_tensor(o, "o"));
-    RT_TRY(check_stat(rho, "rho"));
+    if (rho) RT_TRY(check_stat(rho, "rho"));
     {
         const int64_t nt = tensor_bytes(dims, 2), ns = tensor_bytes(dims, 4) / dims.D;
         RT_TRY(check_no_overlap(o, nt, "o", {{o_sparse, nt}, {resid, nt}, {rho, ns}}, "o_sparse, resid or rho"));

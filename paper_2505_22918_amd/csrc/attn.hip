@@ -398,7 +398,7 @@ void attn_fwd(AttnArgs a) {
 #pragma unroll
     for (int qt = 0; qt < QT; ++qt) {
         const int row = row0 + qt * 32 + l32;
-        rho_r[qt] = (RESHAPE && row < T) ? a.rho[(size_t)bh * T + row] : 0.f;
+        rho_r[qt] = (RESHAPE && a.rho && row < T) ? a.rho[(size_t)bh * T + row] : 0.f;
     }
     // Q^T operands: lane holds query l32 of tile qt, head dims 16s + 8hi .. +7
     // (zero past D and past T)
@@ -848,7 +848,7 @@ void attn_fwd(AttnArgs a) {
             const float rho = split ? li / lf : 1.0f;  // exactly 1 when every block is kept
             if (hi == 0 && row < T && !a.postmask) {
                 const size_t si = (size_t)bh * T + row;
-                a.rho_out[si] = rho;
+                if (a.rho_out) a.rho_out[si] = rho;
                 if (STATS) {
                     if (a.row_max) a.row_max[si] = m_top[qt] * a.scale_nat;
                     if (a.row_sum) a.row_sum[si] = lf * __builtin_amdgcn_exp2f((m_run[qt] - m_top[qt]) * c2);
@@ -866,7 +866,9 @@ void attn_fwd(AttnArgs a) {
                         for (int e = 0; e < 8; ++e) {
                             const float acc = oacc[qt][dt][8 * u + e] * inv;
                             const float osv = (e & 1) ? hi_f(os4[e >> 1]) : lo_f(os4[e >> 1]);
-                            r[e] = split ? acc : 0.f;
+                            // R = O_f - rho O_s (Eq.10); without a ratio output,
+                            // R = O_f - O_s (Eq.10 with rho = 1)
+                            r[e] = split ? (a.rho_out ? acc : __builtin_fmaf(rho - 1.0f, osv, acc)) : 0.f;
                             if (a.postmask) {  // Eq.7: (A o M) V = rho O_s
                                 of[e] = split ? rho * osv : acc;
                             } else {
@@ -895,7 +897,9 @@ void attn_fwd(AttnArgs a) {
         const int row = row0 + rl;
         const float l_tot = pair_sum(l_run[qt]);
         float factor = 1.0f / l_tot;
-        if (RESHAPE) factor *= fminf(1.0f, rho_r[qt] + a.rho_delta);
+        // without a ratio (the ablation with the reshape removed) the sparse
+        // output is added to the residual unscaled
+        if (RESHAPE && a.rho) factor *= fminf(1.0f, rho_r[qt] + a.rho_delta);
         if (STATS && hi == 0 && row < T) {
             const size_t si = (size_t)bh * T + row;
             if (a.row_max) a.row_max[si] = m_top[qt] * a.scale_nat;

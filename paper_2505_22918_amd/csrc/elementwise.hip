@@ -4,6 +4,9 @@
 //                  Eq.10 R   = O_f - rho O_s
 //   reshape_apply  Eq.9 with the ramp and the residual: O = min(1, rho + delta) O_s + R
 //
+// Without a ratio (rho == nullptr, the ablation with the reshape removed) the
+// cache is R = O_f - O_s (Eq.10 with rho = 1) and the output O_s + R.
+//
 // Both are HBM-bound.  Each lane moves 16 bytes per tensor per step (8 bf16 of
 // one row), so a wavefront reads whole 128-byte lines; rows are walked with a
 // grid-stride loop over (row, 16-byte chunk) units.
@@ -39,7 +42,7 @@ constexpr int kUnroll = 4;
 template <int D>
 __device__ __forceinline__ void cache_unit(int64_t row, int ch, const u32x4& f, const u32x4& s, float r,
                                            float* __restrict__ rho, uint16_t* __restrict__ resid) {
-    if (ch == 0) rho[row] = r;
+    if (ch == 0 && rho) rho[row] = r;
     bf16x8 out;
 #pragma unroll
     for (int w = 0; w < 4; ++w) {
@@ -75,7 +78,7 @@ __global__ __launch_bounds__(256) void cache_build_kernel(const uint16_t* __rest
             const size_t off = (size_t)row[j] * D + 8 * ch[j];
             f[j] = ld_stream(of + off);
             s[j] = ld_stream(os + off);
-            r[j] = (ls[row[j]] / lf[row[j]]) * expf(ms[row[j]] - mf[row[j]]);
+            r[j] = rho ? (ls[row[j]] / lf[row[j]]) * expf(ms[row[j]] - mf[row[j]]) : 1.0f;
         }
 #pragma unroll
         for (int j = 0; j < kUnroll; ++j) cache_unit<D>(row[j], ch[j], f[j], s[j], r[j], rho, resid);
@@ -84,7 +87,7 @@ __global__ __launch_bounds__(256) void cache_build_kernel(const uint16_t* __rest
         const int64_t row = u / DC;
         const int ch = (int)(u - row * DC);
         const size_t off = (size_t)row * D + 8 * ch;
-        const float r = (ls[row] / lf[row]) * expf(ms[row] - mf[row]);
+        const float r = rho ? (ls[row] / lf[row]) * expf(ms[row] - mf[row]) : 1.0f;
         cache_unit<D>(row, ch, ld_stream(of + off), ld_stream(os + off), r, rho, resid);
     }
 }
@@ -124,7 +127,7 @@ __global__ __launch_bounds__(256) void reshape_apply_kernel(const uint16_t* __re
             const size_t off = (size_t)row[j] * D + 8 * ch[j];
             s[j] = ld_stream(os + off);
             R[j] = ld_stream(resid + off);
-            r[j] = fminf(1.0f, rho[row[j]] + delta);
+            r[j] = rho ? fminf(1.0f, rho[row[j]] + delta) : 1.0f;
         }
 #pragma unroll
         for (int j = 0; j < kUnroll; ++j) reshape_unit<D>(row[j], ch[j], s[j], R[j], r[j], o);
@@ -133,7 +136,8 @@ __global__ __launch_bounds__(256) void reshape_apply_kernel(const uint16_t* __re
         const int64_t row = u / DC;
         const int ch = (int)(u - row * DC);
         const size_t off = (size_t)row * D + 8 * ch;
-        reshape_unit<D>(row, ch, ld_stream(os + off), ld_stream(resid + off), fminf(1.0f, rho[row] + delta), o);
+        reshape_unit<D>(row, ch, ld_stream(os + off), ld_stream(resid + off),
+                        rho ? fminf(1.0f, rho[row] + delta) : 1.0f, o);
     }
 }
 

@@ -33,14 +33,15 @@ def is_caching_step(t: int, full_steps: int, period: int) -> bool:
     return period > 0 and (t - full_steps + 1) % period == 0
 
 
-def run(mask, qkv, n_steps, full_steps, period, lam, sigma, seed=0, diagnose=True, evolve=None):
+def run(mask, qkv, n_steps, full_steps, period, lam, sigma, seed=0, diagnose=True, evolve=None, ratio=True):
     """Drives n_steps denoising steps of one attention layer.
 
     qkv: device bf16 (q, k, v) of step 0.  Each later step's inputs come from
     ``evolve(prev, t)`` (default: + sigma * N(0,1) drawn on the device from a
-    generator seeded with seed + t, rounded to bf16).  Returns a list of per-step
-    records (and the step outputs when ``diagnose`` is False, for callers that
-    check them).
+    generator seeded with seed + t, rounded to bf16).  ratio=False runs the
+    ablation without the statistical reshape (cache O_full - O_sparse, later
+    steps add it to the sparse output).  Returns a list of per-step records (and
+    the step outputs when ``diagnose`` is False, for callers that check them).
     """
     import torch
 
@@ -53,17 +54,17 @@ def run(mask, qkv, n_steps, full_steps, period, lam, sigma, seed=0, diagnose=Tru
             return tuple((x.float() + sigma * torch.randn(x.shape, generator=g, device=x.device,
                                                           dtype=torch.float32)).to(torch.bfloat16) for x in prev)
 
-    cache = StatCache(mask, full_steps=full_steps, period=period, lam=lam)
+    cache = StatCache(mask, full_steps=full_steps, period=period, lam=lam, ratio=ratio)
     records, outputs = [], []
     cur = qkv
     for t in range(n_steps):
         if t > 0:
             cur = evolve(cur, t)
         q, k, v = cur
-        caching = cache.is_caching_step(t) or cache.rho is None
+        caching = cache.is_caching_step(t) or cache.resid is None
         out = cache.attend(q, k, v, t)
         rec = {"t": t, "kind": ("full" if t < full_steps else "cache") if caching else "reshape"}
-        if not caching:
+        if not caching and ratio:
             rec["rho_delta"] = lam * (t - cache.cached_at)
         if diagnose:
             o_f, rho_t, _ = attn_cache(q, k, v, mask, stats=False)
@@ -73,13 +74,14 @@ def run(mask, qkv, n_steps, full_steps, period, lam, sigma, seed=0, diagnose=Tru
             if caching:
                 rec["out_rel_err_vs_full"] = 0.0
             else:
-                # drift of the cached ratio (from the last caching step) against the
-                # ratio of this step's inputs
-                drift = cache.rho - rho_t
-                rec["rho_cached_mean"] = float(cache.rho.mean())
-                rec["rho_drift_abs_mean"] = float(drift.abs().mean())
-                rec["rho_drift_abs_max"] = float(drift.abs().max())
-                rec["rho_drift_signed_mean"] = float(drift.mean())
+                if cache.rho is not None:
+                    # drift of the cached ratio (from the last caching step) against
+                    # the ratio of this step's inputs
+                    drift = cache.rho - rho_t
+                    rec["rho_cached_mean"] = float(cache.rho.mean())
+                    rec["rho_drift_abs_mean"] = float(drift.abs().mean())
+                    rec["rho_drift_abs_max"] = float(drift.abs().max())
+                    rec["rho_drift_signed_mean"] = float(drift.mean())
                 o_s = attn_sparse(q, k, v, mask, stats=False)
                 rec["out_rel_err_vs_full"] = float(torch.linalg.vector_norm(out.float() - o_f.float()) / nf)
                 rec["sparse_rel_err_vs_full"] = float(torch.linalg.vector_norm(o_s.float() - o_f.float()) / nf)
@@ -98,6 +100,8 @@ def main(argv=None):
     ap.add_argument("--lam", type=float, default=0.0)
     ap.add_argument("--sigma", type=float, default=0.02)
     ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--no-ratio", action="store_true",
+                    help="the ablation without the statistical reshape (residual O_full - O_sparse)")
     args = ap.parse_args(argv)
 
     import numpy as np
@@ -114,7 +118,8 @@ def main(argv=None):
         mask = build_index(wl.T, wl.block, wl.kind, **kw)
     to_dev = lambda b: torch.from_numpy(np.ascontiguousarray(b).view(np.int16)).cuda().view(torch.bfloat16)
     qkv = tuple(to_dev(x) for x in synth.make_qkv(wl, 1, seed=args.seed))
-    recs = run(mask, qkv, args.steps, args.full_steps, args.period, args.lam, args.sigma, seed=args.seed)
+    recs = run(mask, qkv, args.steps, args.full_steps, args.period, args.lam, args.sigma, seed=args.seed,
+               ratio=not args.no_ratio)
     for r in recs:
         print(json.dumps(r), flush=True)
     rs = [r for r in recs if r["kind"] == "reshape"]
@@ -123,7 +128,9 @@ def main(argv=None):
         "lam": args.lam, "sigma": args.sigma,
         "caching_steps": sum(1 for r in recs if r["kind"] != "reshape"),
         "reshape_steps": len(rs),
-        "mean_rho_drift_abs": float(np.mean([r["rho_drift_abs_mean"] for r in rs])) if rs else None,
+        "ratio": not args.no_ratio,
+        "mean_rho_drift_abs": float(np.mean([r["rho_drift_abs_mean"] for r in rs]))
+        if rs and "rho_drift_abs_mean" in rs[0] else None,
         "mean_out_rel_err_reshape": float(np.mean([r["out_rel_err_vs_full"] for r in rs])) if rs else None,
         "mean_out_rel_err_sparse": float(np.mean([r["sparse_rel_err_vs_full"] for r in rs])) if rs else None,
     }

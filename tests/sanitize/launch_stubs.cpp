@@ -33,22 +33,23 @@ hipError_t launch_attention(const AttnArgs& a, int D, int block, AttnMode mode, 
     if (!a.dense) {
         EXPECT(a.row_ptr && a.col_idx && a.nnz > 0 && a.n_masks >= 1);
     }
-    if (mode == kAttnReshape) EXPECT(a.rho && a.resid);
-    if (mode == kAttnCache && !a.postmask) EXPECT(a.rho_out && a.resid_out);
+    if (mode == kAttnReshape) EXPECT(a.resid);  // rho may be absent (no ratio)
+    if (mode == kAttnCache && !a.postmask) EXPECT(a.resid_out);
     return hipSuccess;
 }
 
 hipError_t launch_cache_build(const uint16_t* o_full, const float* m_full, const float* l_full,
                               const uint16_t* o_sparse, const float* m_sparse, const float* l_sparse,
                               int64_t rows, int D, float* rho, uint16_t* resid, hipStream_t) {
-    EXPECT(o_full && m_full && l_full && o_sparse && m_sparse && l_sparse && rho && resid);
+    EXPECT(o_full && o_sparse && resid);
+    if (rho) EXPECT(m_full && l_full && m_sparse && l_sparse);
     EXPECT(rows > 0 && (D == 64 || D == 72));
     return hipSuccess;
 }
 
 hipError_t launch_reshape_apply(const uint16_t* o_sparse, const float* rho, const uint16_t* resid,
                                 float, int64_t rows, int D, uint16_t* o, hipStream_t) {
-    EXPECT(o_sparse && rho && resid && o && rows > 0 && (D == 64 || D == 72));
+    EXPECT(o_sparse && resid && o && rows > 0 && (D == 64 || D == 72));
     return hipSuccess;
 }
 

@@ -143,8 +143,10 @@ def test_attention_argument_errors(lib):
     assert full(FAKE, FAKE, FAKE, d, 48, FAKE, None, None, None) == _lib.RT_EUNSUPPORTED
     assert full(FAKE, None, FAKE, d, 64, FAKE, None, None, None) == _lib.RT_EINVAL
     rs = lib.rt_attn_sparse_reshape
-    assert rs(Q, K, V, d, ctypes.byref(b), None, O2, 0.0, O, None, None, None) == _lib.RT_EINVAL
+    # (a NULL rho is the ratio-free ablation and valid; a misaligned one is not)
+    assert rs(Q, K, V, d, ctypes.byref(b), S1 + 2, O2, 0.0, O, None, None, None) == _lib.RT_EINVAL
     assert "rho" in lib.rt_last_error().decode()
+    assert rs(Q, K, V, d, ctypes.byref(b), None, None, 0.0, O, None, None, None) == _lib.RT_EINVAL
     assert rs(Q, K, V, d, ctypes.byref(b), S1, None, 0.0, O, None, None, None) == _lib.RT_EINVAL
     assert "resid" in lib.rt_last_error().decode()
     assert rs(Q, K, V, d, ctypes.byref(b), S1, O2, float("nan"), O, None, None, None) == _lib.RT_EINVAL
@@ -152,11 +154,13 @@ def test_attention_argument_errors(lib):
     ra = lib.rt_reshape_apply
     assert ra(Q, S1, K, float("inf"), d, O, None) == _lib.RT_EINVAL
     assert "rho_delta" in lib.rt_last_error().decode()
-    assert ra(Q, None, K, 0.0, d, O, None) == _lib.RT_EINVAL
+    assert ra(Q, S1 + 1, K, 0.0, d, O, None) == _lib.RT_EINVAL
     assert "rho" in lib.rt_last_error().decode()
+    assert ra(Q, None, None, 0.0, d, O, None) == _lib.RT_EINVAL
+    assert "resid" in lib.rt_last_error().decode()
     ac = lib.rt_attn_cache
     other = FAKE + 0x100000
-    assert ac(FAKE, FAKE, FAKE, d, ctypes.byref(b), other, None, None, None, FAKE + 0x200000, None) == _lib.RT_EINVAL
+    assert ac(Q, K, V, d, ctypes.byref(b), O, None, None, S1 + 2, O2, None) == _lib.RT_EINVAL
     assert ac(FAKE, FAKE, FAKE, d, ctypes.byref(b), other, None, None, FAKE, None, None) == _lib.RT_EINVAL
     assert ac(FAKE, FAKE, FAKE, d, ctypes.byref(b), other, None, None, FAKE, other, None) == _lib.RT_EINVAL
     assert "alias" in lib.rt_last_error().decode()
@@ -332,3 +336,23 @@ def test_outputs_must_not_overlap_inputs(lib):
     assert lib.rt_cache_build(Q, S1, S2, K, S3, S4, d, S4, O, None) == _lib.RT_EINVAL
     assert lib.rt_cache_build(Q, S1, S2, K, S3, S4, d, O + 16, O, None) == _lib.RT_EINVAL
     assert "overlaps" in lib.rt_last_error().decode()
+
+
+def test_ratio_free_ablation_arguments(lib):
+    # a NULL rho selects the ablation without the reshape; the statistics of
+    # rt_cache_build are then not read, but every other rule still holds
+    d = _dims()
+    b = _bsr()
+    cb = lib.rt_cache_build
+    assert cb(Q, None, None, K, None, None, d, None, None, None) == _lib.RT_EINVAL  # resid missing
+    assert "resid" in lib.rt_last_error().decode()
+    assert cb(Q, None, None, K, None, None, d, None, Q, None) == _lib.RT_EINVAL  # resid overlaps o_full
+    assert "overlaps" in lib.rt_last_error().decode()
+    assert cb(Q, S1, S2, K, S3, None, d, S5, O, None) == _lib.RT_EINVAL  # with rho the statistics are needed
+    ac = lib.rt_attn_cache
+    assert ac(Q, K, V, d, ctypes.byref(b), O, None, None, None, None, None) == _lib.RT_EINVAL
+    assert ac(Q, K, V, d, ctypes.byref(b), O, None, None, None, K, None) == _lib.RT_EINVAL
+    rs = lib.rt_attn_sparse_reshape
+    assert rs(Q, K, V, d, ctypes.byref(b), None, O2, 0.0, O2, None, None, None) == _lib.RT_EINVAL  # o is resid
+    ra = lib.rt_reshape_apply
+    assert ra(Q, None, K, 0.0, d, K, None) == _lib.RT_EINVAL
