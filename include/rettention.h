@@ -147,6 +147,31 @@ rt_status rt_index_size(const rt_pattern* pattern, int32_t T, int32_t block, int
 rt_status rt_index_build(const rt_pattern* pattern, int32_t T, int32_t block, int32_t* row_ptr,
                          int32_t* col_idx, int32_t capacity, void* stream);
 
+/* Dynamic block mask, chosen from the step's own Q and K (the run-time masks
+ * Sec.6 and App. A.2 name as future work, by the block-pooled Q K^T with top-k
+ * selection Sec.2 describes).  Per (batch, head) and query block qb:
+ *   score(qb, kb) = sum_d Qsum_qb[d] * Kmean_kb[d]
+ * Qsum: the fp32 sum of qb's rows, one addition per row in ascending order;
+ * Kmean: kb's rows summed the same way, divided by its token count; the dot
+ * product accumulates in fp32 over ascending d, product and sum each rounded
+ * (no fused multiply-add).  qb keeps itself (Eq.5 needs a non-empty kept set)
+ * and the keep - 1 best other blocks (higher score first, ties to the lower
+ * index, a NaN score last), stored ascending, so every row holds exactly
+ * kk = min(keep, n_qblk) blocks.  The result is one mask per (batch, head):
+ * row_ptr [B*H][n_qblk + 1] (absolute offsets, row (bh, qb) starting at
+ * (bh*n_qblk + qb)*kk) and col_idx [B*H*n_qblk*kk], for an rt_bsr with
+ * n_masks = B*H and nnz = B*H*n_qblk*kk.
+ * q, k: device bf16 [B,H,T,D]; row_ptr, col_idx: device int32 (written);
+ * capacity: entries col_idx can hold (RT_ECAPACITY below nnz); workspace:
+ * caller-owned device memory of at least the bytes rt_dynamic_index_workspace
+ * reports (RT_ECAPACITY otherwise), overwritten; outputs and workspace must not
+ * overlap the inputs or each other.  Needs block in {32, 64}, keep >= 1 and
+ * n_qblk <= 4096. */
+rt_status rt_dynamic_index_workspace(rt_dims dims, int32_t block, int32_t keep, int64_t* bytes);
+rt_status rt_dynamic_index(const void* q, const void* k, rt_dims dims, int32_t block, int32_t keep,
+                           int32_t* row_ptr, int32_t* col_idx, int32_t capacity, void* workspace,
+                           int64_t workspace_bytes, void* stream);
+
 /* Dense attention with row statistics, Eq.1 with the Eq.4 denominator.
  * q, k, v: device bf16 [B,H,T,D]; o: device bf16 [B,H,T,D] (written);
  * row_max, row_sum: device fp32 [B,H,T] (written, either may be NULL).

@@ -5,6 +5,8 @@ memory and launch on torch's current stream; all computation runs in the HIP
 library (the binding only marshals pointers and sizes).
 
   build_index           block CSR of the static mask (Sec.3, App. A.4)
+  dynamic_index         per-(batch, head) mask chosen from the step's Q and K
+                        (block-pooled scores, top-k; Sec.2, Sec.6)
   attn_full             dense attention with row statistics (Eq.1, Eq.4)
   attn_sparse           sparse attention over the block mask (Eq.5)
   cache_build           rho and residual at a caching step (Eq.8, Eq.10)
@@ -29,6 +31,7 @@ __all__ = [
     "BlockMask",
     "index_size",
     "build_index",
+    "dynamic_index",
     "attn_full",
     "attn_sparse",
     "attn_cache",
@@ -218,6 +221,32 @@ def build_index(T, block, kind, device="cuda", host_mask=None, **pat) -> BlockMa
         # keep the mask alive until the build has run on the stream
         torch.cuda.current_stream(row_ptr.device).synchronize()
     return BlockMask(row_ptr, col_idx[:nnz] if nnz else col_idx[:0], int(block), n_blk, int(nnz), n_masks)
+
+
+def dynamic_index(q, k, block, keep) -> BlockMask:
+    """Per-(batch, head) block mask chosen from this step's Q and K: each query
+    block keeps itself and the keep - 1 key blocks whose pooled mean scores best
+    against its pooled query (rt_dynamic_index).  Returns a BlockMask with
+    n_masks = B*H."""
+    torch = _torch()
+    lib = _lib.load()
+    dims = _check_qkv(q, k, k)
+    B, H, T, D = q.shape
+    n_blk = (T + int(block) - 1) // int(block)
+    kk = min(int(keep), n_blk)
+    ws = ctypes.c_int64(0)
+    _lib.check("rt_dynamic_index_workspace", lib.rt_dynamic_index_workspace(dims, int(block), int(keep),
+                                                                            ctypes.byref(ws)))
+    nnz = B * H * n_blk * kk
+    row_ptr = torch.empty(B * H * (n_blk + 1), dtype=torch.int32, device=q.device)
+    col_idx = torch.empty(max(nnz, 1), dtype=torch.int32, device=q.device)
+    work = torch.empty(max(int(ws.value) // 4, 4), dtype=torch.float32, device=q.device)
+    _lib.check("rt_dynamic_index", lib.rt_dynamic_index(_ptr(q), _ptr(k), dims, int(block), int(keep), _ptr(row_ptr),
+                                                        _ptr(col_idx), int(nnz), _ptr(work), int(ws.value),
+                                                        _stream(q)))
+    # `work` returns to torch's stream-ordered cache here; a later reuse on this
+    # stream runs after the launch that reads it
+    return BlockMask(row_ptr, col_idx[:nnz], int(block), n_blk, int(nnz), B * H)
 
 
 def attn_full(q, k, v, block=64, stats=True, out=None):

@@ -18,7 +18,7 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "librettention.so")
-SOURCES = ["attn.hip", "elementwise.hip", "index.hip", "api.cpp"]
+SOURCES = ["attn.hip", "elementwise.hip", "index.hip", "dynamic.hip", "api.cpp"]
 ARCH = "gfx950"
 
 

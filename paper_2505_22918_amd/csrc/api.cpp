@@ -340,6 +340,74 @@ rt_status rt_bsr_check(const rt_bsr* mask, const int32_t* host_row_ptr, const in
     return ok();
 }
 
+namespace {
+
+// Shape checks of the dynamic index build; fills the counts it needs.
+rt_status dynamic_shape(const rt_dims& dims, int32_t block, int32_t keep, int64_t* n_blk, int64_t* kk,
+                        int64_t* nnz, int64_t* ws_bytes) {
+    bool empty = false;
+    RT_TRY(check_dims(dims, &empty));
+    RT_TRY(check_block(block));
+    if (keep < 1) return fail(RT_EINVAL, "keep=%d (need >= 1)", keep);
+    const int64_t nb = ceil_div(dims.T, block);
+    if (nb > 4096) return fail(RT_EUNSUPPORTED, "ceil(T/block)=%lld exceeds 4096 blocks", (long long)nb);
+    const int64_t bh = (int64_t)dims.B * dims.H;
+    *n_blk = nb;
+    *kk = std::min<int64_t>(keep, nb);
+    *nnz = bh * nb * *kk;
+    if (*nnz > INT32_MAX || bh * (nb + 1) > INT32_MAX) return fail(RT_EINVAL, "mask too large for int32 offsets");
+    *ws_bytes = 2 * bh * nb * dims.D * (int64_t)sizeof(float);
+    return RT_OK;
+}
+
+}  // namespace
+
+rt_status rt_dynamic_index_workspace(rt_dims dims, int32_t block, int32_t keep, int64_t* bytes) {
+    if (!bytes) return fail(RT_EINVAL, "bytes is NULL");
+    int64_t nb, kk, nnz, ws;
+    RT_TRY(dynamic_shape(dims, block, keep, &nb, &kk, &nnz, &ws));
+    *bytes = ws;
+    return ok();
+}
+
+rt_status rt_dynamic_index(const void* q, const void* k, rt_dims dims, int32_t block, int32_t keep,
+                           int32_t* row_ptr, int32_t* col_idx, int32_t capacity, void* workspace,
+                           int64_t workspace_bytes, void* stream) {
+    int64_t nb, kk, nnz, ws;
+    RT_TRY(dynamic_shape(dims, block, keep, &nb, &kk, &nnz, &ws));
+    if ((int64_t)dims.B * dims.H * dims.T == 0) return ok();
+    RT_TRY(check_tensor(q, "q"));
+    RT_TRY(check_tensor(k, "k"));
+    RT_TRY(check_stat(row_ptr, "row_ptr"));
+    RT_TRY(check_stat(col_idx, "col_idx"));
+    RT_TRY(check_tensor(workspace, "workspace"));
+    if (capacity < nnz)
+        return fail(RT_ECAPACITY, "capacity=%d but the mask has %lld entries", capacity, (long long)nnz);
+    if (workspace_bytes < ws)
+        return fail(RT_ECAPACITY, "workspace of %lld bytes, %lld needed", (long long)workspace_bytes, (long long)ws);
+    const int64_t nt = tensor_bytes(dims, 2);
+    const int64_t nrp = (int64_t)dims.B * dims.H * (nb + 1) * 4, nci = nnz * 4;
+    RT_TRY(check_no_overlap(row_ptr, nrp, "row_ptr", {{q, nt}, {k, nt}, {col_idx, nci}, {workspace, ws}},
+                            "q, k, col_idx or the workspace"));
+    RT_TRY(check_no_overlap(col_idx, nci, "col_idx", {{q, nt}, {k, nt}, {workspace, ws}}, "q, k or the workspace"));
+    RT_TRY(check_no_overlap(workspace, ws, "workspace", {{q, nt}, {k, nt}}, "q or k"));
+    rt::DynIndexArgs a{};
+    a.q = static_cast<const uint16_t*>(q);
+    a.k = static_cast<const uint16_t*>(k);
+    a.B = dims.B;
+    a.H = dims.H;
+    a.T = dims.T;
+    a.D = dims.D;
+    a.block = block;
+    a.n_blk = (int32_t)nb;
+    a.keep = keep;
+    a.qsum = static_cast<float*>(workspace);
+    a.kmean = a.qsum + (size_t)dims.B * dims.H * nb * dims.D;
+    a.row_ptr = row_ptr;
+    a.col_idx = col_idx;
+    return hip_status(rt::launch_dynamic_index(a, static_cast<hipStream_t>(stream)), "dynamic index launch");
+}
+
 rt_status rt_attn_full(const void* q, const void* k, const void* v, rt_dims dims, int32_t block, void* o,
                        float* row_max, float* row_sum, void* stream) {
     bool empty = false;

@@ -66,4 +66,20 @@ struct IndexArgs {
 
 hipError_t launch_index_build(const IndexArgs& a, hipStream_t stream);
 
+// Dynamic block mask from the step's Q and K (dynamic.hip): workspace qsum and
+// kmean [B*H][n_blk][D] fp32; row_ptr [B*H][n_blk + 1], col_idx [B*H*n_blk*kk]
+// with kk = min(keep, n_blk).
+struct DynIndexArgs {
+    const uint16_t* q;  // bf16 [B,H,T,D]
+    const uint16_t* k;
+    int32_t B, H, T, D;
+    int32_t block, n_blk, keep;
+    float* qsum;
+    float* kmean;
+    int32_t* row_ptr;
+    int32_t* col_idx;
+};
+
+hipError_t launch_dynamic_index(const DynIndexArgs& a, hipStream_t stream);
+
 }  // namespace rt

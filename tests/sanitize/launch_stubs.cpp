@@ -60,4 +60,11 @@ hipError_t launch_index_build(const IndexArgs& a, hipStream_t) {
     return hipSuccess;
 }
 
+hipError_t launch_dynamic_index(const DynIndexArgs& a, hipStream_t) {
+    EXPECT(a.q && a.k && a.qsum && a.kmean && a.row_ptr && a.col_idx);
+    EXPECT(a.T > 0 && a.n_blk == (a.T + a.block - 1) / a.block && a.n_blk <= 4096 && a.keep >= 1);
+    EXPECT(a.kmean == a.qsum + (size_t)a.B * a.H * a.n_blk * a.D);
+    return hipSuccess;
+}
+
 }  // namespace rt

@@ -356,3 +356,30 @@ def test_ratio_free_ablation_arguments(lib):
     assert rs(Q, K, V, d, ctypes.byref(b), None, O2, 0.0, O2, None, None, None) == _lib.RT_EINVAL  # o is resid
     ra = lib.rt_reshape_apply
     assert ra(Q, None, K, 0.0, d, K, None) == _lib.RT_EINVAL
+
+
+def test_dynamic_index_argument_errors(lib):
+    d = _dims()  # B1 H2 T256 D64: 4 blocks of 64, workspace 2*2*4*64*4 = 4 KiB
+    ws = ctypes.c_int64(0)
+    assert lib.rt_dynamic_index_workspace(d, 64, 2, ctypes.byref(ws)) == _lib.RT_OK
+    assert ws.value == 2 * 2 * 4 * 64 * 4
+    assert lib.rt_dynamic_index_workspace(d, 64, 2, None) == _lib.RT_EINVAL
+    assert lib.rt_dynamic_index_workspace(d, 48, 2, ctypes.byref(ws)) == _lib.RT_EUNSUPPORTED
+    assert lib.rt_dynamic_index_workspace(d, 64, 0, ctypes.byref(ws)) == _lib.RT_EINVAL
+    assert lib.rt_dynamic_index_workspace(_dims(T=4097 * 32), 32, 2, ctypes.byref(ws)) == _lib.RT_EUNSUPPORTED
+    assert lib.rt_dynamic_index_workspace(_dims(D=80), 64, 2, ctypes.byref(ws)) == _lib.RT_EUNSUPPORTED
+    di = lib.rt_dynamic_index
+    RP, CI, WS = S1, S2, S3  # row_ptr 40 B, col_idx 64 B, workspace 4 KiB: disjoint
+    nnz = 2 * 4 * 2
+    assert di(Q, K, d, 64, 2, RP, CI, nnz - 1, WS, 4096, None) == _lib.RT_ECAPACITY
+    assert di(Q, K, d, 64, 2, RP, CI, nnz, WS, 4095, None) == _lib.RT_ECAPACITY
+    assert "workspace" in lib.rt_last_error().decode()
+    assert di(None, K, d, 64, 2, RP, CI, nnz, WS, 4096, None) == _lib.RT_EINVAL
+    assert di(Q, K, d, 64, 2, RP + 2, CI, nnz, WS, 4096, None) == _lib.RT_EINVAL
+    assert di(Q, K, d, 64, 2, RP, CI, nnz, WS + 4, 4096, None) == _lib.RT_EINVAL
+    assert di(Q, K, d, 64, 2, RP, CI, nnz, None, 4096, None) == _lib.RT_EINVAL
+    assert di(Q, K, d, 64, 2, RP, RP + 16, nnz, WS, 4096, None) == _lib.RT_EINVAL  # col_idx overlaps row_ptr
+    assert "overlaps" in lib.rt_last_error().decode()
+    assert di(Q, K, d, 64, 2, RP, CI, nnz, K, 4096, None) == _lib.RT_EINVAL  # workspace is k
+    assert di(Q, K, d, 64, 2, Q + 64, CI, nnz, WS, 4096, None) == _lib.RT_EINVAL  # row_ptr inside q
+    assert di(Q, K, d, 64, 0, RP, CI, nnz, WS, 4096, None) == _lib.RT_EINVAL
