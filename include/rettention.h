@@ -172,6 +172,18 @@ rt_status rt_dynamic_index(const void* q, const void* k, rt_dims dims, int32_t b
                            int32_t* row_ptr, int32_t* col_idx, int32_t capacity, void* workspace,
                            int64_t workspace_bytes, void* stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph capture,
+ * tight serving loops, harnesses that forbid allocation): rt_dynamic_index
+ * with its workspace taken from a library-owned device array of 16 MiB per
+ * GPU instead of an argument; nothing is allocated.  The shape's workspace
+ * (2*B*H*n_qblk*D fp32) must fit it, else RT_ECAPACITY.  The array's address
+ * is looked up on the first call on each device (RT_EHIP if that fails).
+ * Every call on one GPU shares that GPU's array: calls that overlap on one GPU
+ * (on different streams or threads) race; calls on one stream do not.  Nothing
+ * in it needs clearing between calls. */
+rt_status rt_dynamic_index_noalloc(const void* q, const void* k, rt_dims dims, int32_t block, int32_t keep,
+                                   int32_t* row_ptr, int32_t* col_idx, int32_t capacity, void* stream);
+
 /* Dense attention with row statistics, Eq.1 with the Eq.4 denominator.
  * q, k, v: device bf16 [B,H,T,D]; o: device bf16 [B,H,T,D] (written);
  * row_max, row_sum: device fp32 [B,H,T] (written, either may be NULL).

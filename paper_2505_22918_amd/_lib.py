@@ -56,6 +56,8 @@ class RtPattern(ctypes.Structure):
 _SIGS = {
     "rt_bsr_check": (c_int32, [ctypes.POINTER(RtBsr), c_void_p, c_void_p]),
     "rt_dynamic_index_workspace": (c_int32, [RtDims, c_int32, c_int32, ctypes.POINTER(ctypes.c_int64)]),
+    "rt_dynamic_index_noalloc": (c_int32, [c_void_p, c_void_p, RtDims, c_int32, c_int32, c_void_p, c_void_p,
+                                           c_int32, c_void_p]),
     "rt_dynamic_index": (c_int32, [c_void_p, c_void_p, RtDims, c_int32, c_int32, c_void_p, c_void_p, c_int32,
                                    c_void_p, ctypes.c_int64, c_void_p]),
     "rt_index_size": (c_int32, [ctypes.POINTER(RtPattern), c_int32, c_int32, ctypes.POINTER(c_int32)]),

@@ -370,6 +370,19 @@ rt_status rt_dynamic_index_workspace(rt_dims dims, int32_t block, int32_t keep, 
     return ok();
 }
 
+rt_status rt_dynamic_index_noalloc(const void* q, const void* k, rt_dims dims, int32_t block, int32_t keep,
+                                   int32_t* row_ptr, int32_t* col_idx, int32_t capacity, void* stream) {
+    int64_t nb, kk, nnz, ws;
+    RT_TRY(dynamic_shape(dims, block, keep, &nb, &kk, &nnz, &ws));
+    if (ws > rt::kDynScratchFloats * (int64_t)sizeof(float))
+        return fail(RT_ECAPACITY, "the shape needs %lld workspace bytes, the allocation-free build holds %lld",
+                    (long long)ws, (long long)(rt::kDynScratchFloats * (int64_t)sizeof(float)));
+    if ((int64_t)dims.B * dims.H * dims.T == 0) return ok();
+    float* scratch = nullptr;
+    RT_TRY(hip_status(rt::dynamic_scratch(&scratch), "workspace address"));
+    return rt_dynamic_index(q, k, dims, block, keep, row_ptr, col_idx, capacity, scratch, ws, stream);
+}
+
 rt_status rt_dynamic_index(const void* q, const void* k, rt_dims dims, int32_t block, int32_t keep,
                            int32_t* row_ptr, int32_t* col_idx, int32_t capacity, void* workspace,
                            int64_t workspace_bytes, void* stream) {

@@ -26,6 +26,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <atomic>
+
 #include "kernels.h"
 
 #pragma clang fp contract(off)
@@ -131,7 +133,35 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(const float* __rest
     }
 }
 
+constexpr int kMaxDevices = 64;
+std::atomic<float*> g_scratch_ptr[kMaxDevices];
+
 }  // namespace
+
+// Library-owned workspace of rt_dynamic_index_noalloc, for callers that cannot
+// allocate: the pooled query sums and key means, 2 * B*H*n_blk*D floats at most
+// kDynScratchFloats (16 MiB).  Each GPU holds its own copy until the process
+// ends.  In host code `scratch` names a host-side stand-in, never the device
+// memory: its device address comes from hipGetSymbolAddress, once per device.
+static __device__ __align__(256) float scratch[kDynScratchFloats];
+
+hipError_t dynamic_scratch(float** ptr) {
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+    float* p = g_scratch_ptr[dev].load(std::memory_order_acquire);
+    if (p == nullptr) {
+        // first call on this device, with it current: its copy's address
+        void* addr = nullptr;
+        e = hipGetSymbolAddress(&addr, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        p = static_cast<float*>(addr);
+        g_scratch_ptr[dev].store(p, std::memory_order_release);
+    }
+    *ptr = p;
+    return hipSuccess;
+}
 
 hipError_t launch_dynamic_index(const DynIndexArgs& a, hipStream_t stream) {
     const int n_bh = a.B * a.H;

@@ -82,4 +82,9 @@ struct DynIndexArgs {
 
 hipError_t launch_dynamic_index(const DynIndexArgs& a, hipStream_t stream);
 
+// The library-owned workspace of the allocation-free dynamic index build: the
+// device address of this GPU's copy (looked up on the first call on a device).
+constexpr int64_t kDynScratchFloats = (int64_t)4 << 20;  // 16 MiB
+hipError_t dynamic_scratch(float** ptr);
+
 }  // namespace rt

@@ -67,4 +67,10 @@ hipError_t launch_dynamic_index(const DynIndexArgs& a, hipStream_t) {
     return hipSuccess;
 }
 
+hipError_t dynamic_scratch(float** ptr) {
+    static float stand_in[4];  // the sanitizer build never launches, so no device memory is needed
+    *ptr = stand_in;
+    return hipSuccess;
+}
+
 }  // namespace rt
