@@ -46,8 +46,13 @@ __all__ = [
 def f32_to_bf16_bits(x):
     """Round float32 to bfloat16 (round to nearest, ties to even); returns uint16 bits."""
     x = np.ascontiguousarray(x, dtype=np.float32)
-    u = x.view(np.uint32).astype(np.uint64)
-    r = (u + 0x7FFF + ((u >> 16) & 1)) >> 16
+    u = x.view(np.uint32)
+    # in uint32 the sum wraps past 2^32 only where the 64-bit sum would carry
+    # into bit 32, which the truncation to 16 bits drops either way
+    r = (u >> 16) & np.uint32(1)
+    r += np.uint32(0x7FFF)
+    r += u
+    r >>= np.uint32(16)
     return r.astype(np.uint16)
 
 
