@@ -348,7 +348,30 @@ def main():
                                  stream)
         else:
             t_index = time_calls(lambda: rt.build_index(wl.T, wl.block, wl.kind, device=dev, **kw), 3, stream)
+        # the ablation without the statistical reshape: the one-pass caching step
+        # caches R' = O_full - O_sparse, the fused call returns O_sparse + R'
+        _, _, resid_nr = rt.attn_cache(q1, k1, v1, mask, stats=False, ratio=False)
+        t_nr_cache = time_calls(lambda: rt.attn_cache(q1, k1, v1, mask, stats=False, ratio=False, out=out), 3,
+                                stream)
+        t_nr_fused = time_calls(lambda: rt.attn_sparse_reshape(q2, k2, v2, mask, None, resid_nr, 0.0, out=out),
+                                args.steps, stream)
+        del resid_nr
+        # dynamic block masks at this shape, keeping as many blocks per row as the
+        # static mask's longest row, and the fused call over them
+        keep_dyn = int(np.diff(rp).max())
+        dyn = rt.dynamic_index(q1, k1, wl.block, keep_dyn)
+        t_dyn = time_calls(lambda: rt.dynamic_index(q1, k1, wl.block, keep_dyn), 10, stream)
+        t_dyn_fused = time_calls(lambda: rt.attn_sparse_reshape(q2, k2, v2, dyn, rho, resid, 0.0, out=out),
+                                 args.steps, stream)
         n = wl.B * wl.H * wl.T
+        # dynamic index bytes: Q and K read once (bf16), pooled sums and means
+        # written and read (fp32), the CSR written
+        dyn_bytes = 2 * n * wl.D * 2 + 2 * 2 * wl.B * wl.H * dyn.n_qblk * wl.D * 4 + 4 * (dyn.nnz + dyn.row_ptr.numel())
+        drp, dci = dyn.row_ptr.cpu().numpy(), dyn.col_idx.cpu().numpy()
+        dyn_flops = 0.0
+        for m in range(wl.B * wl.H):  # each (batch, head) has its own mask
+            hrp = drp[m * (wl.n_blk + 1):(m + 1) * (wl.n_blk + 1)]
+            dyn_flops += kept_flops(wl, hrp - hrp[0], dci[hrp[0]:hrp[-1]]) / (wl.B * wl.H)
         ew_bytes = 2 * n * wl.D * 3 + 4 * n
         cache_bytes = 2 * n * wl.D * 3 + 4 * n * 5
         path = {
@@ -364,6 +387,13 @@ def main():
             "caching_step_three_calls_ms": round(t_full_stats + t_sparse + t_cache, 4),
             "caching_step_one_pass_ms": round(t_onepass, 4),
             "speedup_vs_dense": round(t_dense / ms_call, 2),
+            "ablation_caching_one_pass_ms": round(t_nr_cache, 4),
+            "ablation_fused_ms": round(t_nr_fused, 4),
+            "dynamic_index_keep": keep_dyn,
+            "dynamic_index_ms": round(t_dyn, 4),
+            "dynamic_index_gbs": round(dyn_bytes / (t_dyn * 1e-3) / 1e9, 1),
+            "fused_over_dynamic_mask_ms": round(t_dyn_fused, 4),
+            "fused_over_dynamic_mask_tflops": round(dyn_flops / (t_dyn_fused * 1e-3) / 1e12, 2),
         }
         log(f"path: {path}")
 
