@@ -15,13 +15,21 @@
 // a NaN score ranked last); rows are stored ascending.  Every fp32 operation is
 // fixed, so the choice is reproducible bit for bit.
 //
-//   pool_kernel    one workgroup per (batch, head, block): lane d < D sums the
-//                  block's Q rows, lane 128 + d its K rows; the K sum is divided
-//                  by the token count.  Writes qsum and kmean [B*H][n_blk][D].
-//   select_kernel  one workgroup per (batch, head, query block): every key
-//                  block's score into LDS, each candidate's rank among the other
-//                  blocks, then the kept blocks in ascending order at the row's
-//                  closed-form offset (every row keeps exactly min(keep, n_blk)).
+//   pool_kernel    one workgroup per (batch, head, block): the block's Q and K
+//                  rows are staged in LDS with 16-byte loads, then lane d < D
+//                  sums Q column d over the rows in ascending order and lane
+//                  128 + d does the same for K and divides by the token count.
+//                  Writes qsum and kmean [B*H][n_blk][D].
+//   select_kernel  one workgroup per (batch, head) and `rows` consecutive
+//                  query blocks (4, or 2 above 2048 blocks, so that the
+//                  scores fit 32 KB of LDS): the key means pass through LDS in chunks of
+//                  kSelChunk blocks (one 16-byte load per lane and round), each
+//                  lane scoring one (query block, key block) pair of the chunk;
+//                  then, row by row, a radix selection of the keep - 1 best
+//                  other blocks (independent of keep: four histogram passes
+//                  over the candidates) and the kept blocks in ascending order
+//                  at the row's closed-form offset (every row keeps exactly
+//                  min(keep, n_blk)).
 
 #include <hip/hip_runtime.h>
 #include <stdint.h>
@@ -37,25 +45,46 @@ namespace {
 
 constexpr int kPoolThreads = 256;
 constexpr int kSelThreads = 256;
-constexpr int kMaxDynBlocks = 4096;
+constexpr int kSelRows = 4;                         // most query blocks per select workgroup
+constexpr int kSelChunk = kSelThreads / kSelRows;  // key blocks per LDS chunk
+constexpr int kSelScoreBytes = 32 << 10;           // LDS for the scores of one workgroup
+static_assert(kSelThreads == 256, "one radix bin per thread");
+constexpr int kMaxD = 72;
+constexpr int kPoolRows = 64;                      // largest block
 
 __device__ __forceinline__ float bf16_to_f32(uint16_t b) { return __uint_as_float((uint32_t)b << 16); }
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 __global__ __launch_bounds__(kPoolThreads) void pool_kernel(const uint16_t* __restrict__ q,
                                                             const uint16_t* __restrict__ k, int T, int D,
                                                             int block, int n_blk, float* __restrict__ qsum,
                                                             float* __restrict__ kmean) {
+    // the block's rows of Q, then of K, row-major as in HBM (2D bytes per row)
+    __shared__ __attribute__((aligned(16))) uint16_t tile[2][kPoolRows * kMaxD];
     const int bh = blockIdx.x / n_blk;
     const int b = blockIdx.x - bh * n_blk;
     const int t = threadIdx.x;
+    const int r0 = b * block;
+    const int cnt = min(block, T - r0);
+    const size_t base = ((size_t)bh * T + r0) * D;
+    // 16-byte pieces of the block's rows: cnt * D / 8 per tensor (D is a multiple of 8)
+    const int n16 = cnt * D / 8;
+    const u32x4* qs = reinterpret_cast<const u32x4*>(q + base);
+    const u32x4* ks = reinterpret_cast<const u32x4*>(k + base);
+    u32x4* tq = reinterpret_cast<u32x4*>(tile[0]);
+    u32x4* tk = reinterpret_cast<u32x4*>(tile[1]);
+    for (int i = t; i < n16; i += kPoolThreads) {
+        tq[i] = qs[i];
+        tk[i] = ks[i];
+    }
+    __syncthreads();
     const bool is_q = t < 128;
     const int d = is_q ? t : t - 128;
     if (d >= D) return;
-    const int r0 = b * block;
-    const int cnt = min(block, T - r0);
-    const uint16_t* src = (is_q ? q : k) + ((size_t)bh * T + r0) * D + d;
+    const uint16_t* col = tile[is_q ? 0 : 1] + d;
     float acc = 0.0f;
-    for (int r = 0; r < cnt; ++r) acc = __fadd_rn(acc, bf16_to_f32(src[(size_t)r * D]));
+    for (int r = 0; r < cnt; ++r) acc = __fadd_rn(acc, bf16_to_f32(col[r * D]));
     const size_t o = ((size_t)bh * n_blk + b) * D + d;
     if (is_q) {
         qsum[o] = acc;
@@ -64,72 +93,179 @@ __global__ __launch_bounds__(kPoolThreads) void pool_kernel(const uint16_t* __re
     }
 }
 
-// a > b in the selection order: higher score first, a NaN score last, then the
-// lower block index
-__device__ __forceinline__ bool before(float sa, int a, float sb, int b) {
-    const float xa = sa != sa ? -INFINITY : sa;
-    const float xb = sb != sb ? -INFINITY : sb;
-    return xa > xb || (xa == xb && a < b);
+// Selection order as one unsigned key, larger = better: a NaN score counts as
+// -inf and -0 as +0 (so keys are equal exactly when the fp32 scores compare
+// equal), and the float's bits are mapped so that unsigned order is numeric
+// order.  Equal keys go to the lower block index.
+__device__ __forceinline__ uint32_t order_key(float x) {
+    if (x != x) x = -INFINITY;
+    if (x == 0.0f) x = 0.0f;
+    const uint32_t u = __float_as_uint(x);
+    return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+// Exclusive prefix sum of v over the workgroup's kSelThreads lanes (thread
+// order); *total receives the sum.  Two barriers; every thread must call it.
+__device__ __forceinline__ int group_excl_scan(int v, int* wsum, int* total) {
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    int x = v;
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+        const int y = __shfl_up(x, d, 64);
+        if (lane >= d) x += y;
+    }
+    if (lane == 63) wsum[w] = x;
+    __syncthreads();
+    int off = 0, tot = 0;
+#pragma unroll
+    for (int i = 0; i < kSelThreads / 64; ++i) {
+        const int sw = wsum[i];
+        off += i < w ? sw : 0;
+        tot += sw;
+    }
+    __syncthreads();  // wsum may be reused
+    *total = tot;
+    return off + x - v;
 }
 
 __global__ __launch_bounds__(kSelThreads) void select_kernel(const float* __restrict__ qsum,
                                                              const float* __restrict__ kmean, int D, int n_blk,
-                                                             int keep, int32_t* __restrict__ row_ptr,
+                                                             int keep, int rows, int32_t* __restrict__ row_ptr,
                                                              int32_t* __restrict__ col_idx) {
-    __shared__ float sc[kMaxDynBlocks];
-    __shared__ float qv[128];
-    __shared__ int part[kSelThreads + 1];
-    const int bh = blockIdx.x / n_blk;
-    const int qb = blockIdx.x - bh * n_blk;
+    // scores of the workgroup's rows: rows x n_blk floats of dynamic LDS
+    extern __shared__ float sc[];
+    __shared__ float qv[kSelRows][kMaxD];  // pooled queries of the rows
+    // one chunk of key means, rows padded by one float so that the lanes of a
+    // wave, reading one head dim of 64 consecutive key blocks, hit 64 banks
+    __shared__ float km[kSelChunk * (kMaxD + 1)];
+    const int n_grp = (n_blk + rows - 1) / rows;
+    const int bh = blockIdx.x / n_grp;
+    const int qb0 = (blockIdx.x - bh * n_grp) * rows;
     const int tid = threadIdx.x;
     const int kk = keep < n_blk ? keep : n_blk;
-    if (tid < D) qv[tid] = qsum[((size_t)bh * n_blk + qb) * D + tid];
-    __syncthreads();
-    for (int kb = tid; kb < n_blk; kb += kSelThreads) {
-        const float* km = kmean + ((size_t)bh * n_blk + kb) * D;
-        float s = 0.0f;
-        for (int d = 0; d < D; ++d) s = __fadd_rn(s, __fmul_rn(qv[d], km[d]));
-        sc[kb] = s;
+    const int kst = D + 1;  // LDS row stride of km
+    for (int i = tid; i < rows * D; i += kSelThreads) {
+        const int r = i / D, d = i - r * D;
+        qv[r][d] = qb0 + r < n_blk ? qsum[((size_t)bh * n_blk + qb0 + r) * D + d] : 0.0f;
+    }
+    const float* kh = kmean + (size_t)bh * n_blk * D;
+    const int pr = tid / kSelChunk;  // the pair this lane scores: row pr,
+    const int pc = tid - pr * kSelChunk;  // key block c0 + pc
+    for (int c0 = 0; c0 < n_blk; c0 += kSelChunk) {
+        const int nc = n_blk - c0 < kSelChunk ? n_blk - c0 : kSelChunk;
+        __syncthreads();  // the previous chunk's scores are done (and qv is in)
+        // the chunk's nc * D floats are contiguous in HBM: 16-byte loads
+        const int n16 = nc * D / 4;
+        const u32x4* src = reinterpret_cast<const u32x4*>(kh + (size_t)c0 * D);
+        for (int i = tid; i < n16; i += kSelThreads) {
+            const u32x4 v = src[i];
+            const int e = 4 * i, r = e / D, d = e - r * D;  // D is a multiple of 4
+            float* dst = km + r * kst + d;
+            dst[0] = __uint_as_float(v[0]);
+            dst[1] = __uint_as_float(v[1]);
+            dst[2] = __uint_as_float(v[2]);
+            dst[3] = __uint_as_float(v[3]);
+        }
+        __syncthreads();
+        if (pr < rows && pc < nc) {
+            const float* kv = km + pc * kst;
+            float s = 0.0f;
+            for (int d = 0; d < D; ++d) s = __fadd_rn(s, __fmul_rn(qv[pr][d], kv[d]));
+            sc[pr * n_blk + c0 + pc] = s;
+        }
     }
     __syncthreads();
-    // each thread owns a contiguous run of candidate blocks; a block is kept when
-    // it is the diagonal or ranks among the keep - 1 best other blocks
+    // Selection, row by row.  Each thread owns a contiguous run of at most 16
+    // candidate blocks.  The keep - 1 best blocks other than the diagonal are
+    // found by radix selection on the 32-bit keys: four passes of 8-bit digits,
+    // from the top, narrow the key of the (keep-1)-th best block (the
+    // threshold) and how many blocks holding exactly that key are kept; those
+    // go to the lowest indices.  Every block with a larger key is kept.
+    __shared__ int hist[256];
+    __shared__ int wsum[kSelThreads / 64];
+    __shared__ int pick[2];
     const int seg = (n_blk + kSelThreads - 1) / kSelThreads;
-    const int c0 = tid * seg < n_blk ? tid * seg : n_blk;
-    const int c1 = c0 + seg < n_blk ? c0 + seg : n_blk;
-    unsigned long long kept_bits = 0;  // bit i: candidate c0 + i is kept (seg <= 16)
-    int n_kept = 0;
-    for (int c = c0; c < c1; ++c) {
-        bool kept = c == qb;
-        if (!kept && kk > 1) {
-            int rank = 0;
-            const float s = sc[c];
-            for (int o = 0; o < n_blk && rank < kk - 1; ++o) rank += (o != qb && o != c && before(sc[o], o, s, c));
-            kept = rank < kk - 1;
+    const int c_lo = tid * seg < n_blk ? tid * seg : n_blk;
+    const int c_hi = c_lo + seg < n_blk ? c_lo + seg : n_blk;
+    const int need = kk - 1;  // other blocks to keep, < n_blk
+    for (int r = 0; r < rows; ++r) {
+        const int qb = qb0 + r;
+        if (qb >= n_blk) break;  // uniform over the workgroup
+        const float* row = sc + r * n_blk;
+        uint32_t key[16];
+#pragma unroll
+        for (int i = 0; i < 16; ++i) key[i] = c_lo + i < c_hi ? order_key(row[c_lo + i]) : 0u;
+        uint32_t thr = 0, thr_mask = 0;  // digits of the threshold found so far
+        int rem = need;                   // blocks still to keep at the threshold
+        if (need > 0 && need < n_blk - 1) {
+            for (int shift = 24; shift >= 0; shift -= 8) {
+                hist[tid] = 0;  // kSelThreads == 256 bins
+                __syncthreads();
+#pragma unroll
+                for (int i = 0; i < 16; ++i) {
+                    const int c = c_lo + i;
+                    if (c < c_hi && c != qb && (key[i] & thr_mask) == thr) atomicAdd(&hist[(key[i] >> shift) & 255u], 1);
+                }
+                __syncthreads();
+                // bins from the top: S(t) blocks have digit >= t; the threshold's
+                // digit is the t with S(t+1) < rem <= S(t)
+                const int h = hist[tid];
+                int tot;
+                const int below = group_excl_scan(h, wsum, &tot);
+                const int s_t = tot - below;
+                if (h > 0 && s_t >= rem && s_t - h < rem) {
+                    pick[0] = tid;
+                    pick[1] = rem - (s_t - h);
+                }
+                __syncthreads();
+                thr |= (uint32_t)pick[0] << shift;
+                thr_mask |= 255u << shift;
+                rem = pick[1];
+            }
         }
-        if (kept) {
-            kept_bits |= 1ull << (c - c0);
-            ++n_kept;
+        // ties at the threshold in ascending block order: this thread's first
+        // tie is number `tie0` among them
+        int n_tie = 0;
+#pragma unroll
+        for (int i = 0; i < 16; ++i) n_tie += (c_lo + i < c_hi && c_lo + i != qb && key[i] == thr) ? 1 : 0;
+        int tot_tie;
+        int tie = group_excl_scan(n_tie, wsum, &tot_tie);
+        unsigned kept_bits = 0;  // bit i: candidate c_lo + i is kept
+        int n_kept = 0;
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+            const int c = c_lo + i;
+            if (c >= c_hi) continue;
+            bool kept;
+            if (c == qb || need >= n_blk - 1) {
+                kept = true;
+            } else if (need == 0) {
+                kept = false;
+            } else if (key[i] == thr) {
+                kept = tie < rem;
+                ++tie;
+            } else {
+                kept = key[i] > thr;
+            }
+            if (kept) {
+                kept_bits |= 1u << i;
+                ++n_kept;
+            }
         }
-    }
-    part[tid + 1] = n_kept;
-    if (tid == 0) part[0] = 0;
-    __syncthreads();
-    if (tid == 0) {
-        for (int i = 1; i <= kSelThreads; ++i) part[i] += part[i - 1];
-    }
-    __syncthreads();
-    const size_t row_off = ((size_t)bh * n_blk + qb) * kk;
-    int pos = part[tid];
-    for (int c = c0; c < c1; ++c) {
-        if ((kept_bits >> (c - c0)) & 1ull) {
-            if (pos < kk) col_idx[row_off + pos] = c;  // exactly kk kept per row (total order)
-            ++pos;
+        int tot_kept;
+        int pos = group_excl_scan(n_kept, wsum, &tot_kept);  // == kk (total order)
+        const size_t row_off = ((size_t)bh * n_blk + qb) * kk;
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+            if ((kept_bits >> i) & 1u) {
+                if (pos < kk) col_idx[row_off + pos] = c_lo + i;
+                ++pos;
+            }
         }
-    }
-    if (tid == 0) {
-        row_ptr[(size_t)bh * (n_blk + 1) + qb] = (int32_t)row_off;
-        if (qb == n_blk - 1) row_ptr[(size_t)bh * (n_blk + 1) + n_blk] = (int32_t)(row_off + kk);
+        if (tid == 0) {
+            row_ptr[(size_t)bh * (n_blk + 1) + qb] = (int32_t)row_off;
+            if (qb == n_blk - 1) row_ptr[(size_t)bh * (n_blk + 1) + n_blk] = (int32_t)(row_off + kk);
+        }
     }
 }
 
@@ -169,8 +305,12 @@ hipError_t launch_dynamic_index(const DynIndexArgs& a, hipStream_t stream) {
                        a.block, a.n_blk, a.qsum, a.kmean);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(select_kernel, dim3(n_bh * a.n_blk), dim3(kSelThreads), 0, stream, a.qsum, a.kmean, a.D,
-                       a.n_blk, a.keep, a.row_ptr, a.col_idx);
+    int rows = kSelRows;
+    while (rows > 1 && (size_t)rows * a.n_blk * sizeof(float) > (size_t)kSelScoreBytes) rows /= 2;
+    const int n_grp = (a.n_blk + rows - 1) / rows;
+    const size_t lds = (size_t)rows * a.n_blk * sizeof(float);
+    hipLaunchKernelGGL(select_kernel, dim3(n_bh * n_grp), dim3(kSelThreads), lds, stream, a.qsum, a.kmean, a.D,
+                       a.n_blk, a.keep, rows, a.row_ptr, a.col_idx);
     return hipGetLastError();
 }
 

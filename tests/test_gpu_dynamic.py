@@ -24,6 +24,7 @@ SHAPES = [
     (2, 2, 45, 72, 32, 1),
     (1, 2, 700, 64, 64, 99),   # keep beyond the block count: every block
     (2, 16, 1024, 72, 32, 2),  # PixArt-alpha-512 shape
+    (1, 1, 2100 * 32 - 5, 72, 32, 3),  # 2100 blocks: two query blocks per select workgroup, ragged tail
 ]
 
 
