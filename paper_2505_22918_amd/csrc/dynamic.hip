@@ -25,11 +25,11 @@
 //                  scores fit 32 KB of LDS): the key means pass through LDS in chunks of
 //                  kSelChunk blocks (one 16-byte load per lane and round), each
 //                  lane scoring one (query block, key block) pair of the chunk;
-//                  then, row by row, a radix selection of the keep - 1 best
-//                  other blocks (independent of keep: four histogram passes
-//                  over the candidates) and the kept blocks in ascending order
-//                  at the row's closed-form offset (every row keeps exactly
-//                  min(keep, n_blk)).
+//                  then one wave per row: a radix selection of the keep - 1
+//                  best other blocks (independent of keep: four histogram
+//                  passes over the candidates) and the kept blocks in
+//                  ascending order at the row's closed-form offset (every row
+//                  keeps exactly min(keep, n_blk)).
 
 #include <hip/hip_runtime.h>
 #include <stdint.h>
@@ -48,7 +48,7 @@ constexpr int kSelThreads = 256;
 constexpr int kSelRows = 4;                         // most query blocks per select workgroup
 constexpr int kSelChunk = kSelThreads / kSelRows;  // key blocks per LDS chunk
 constexpr int kSelScoreBytes = 32 << 10;           // LDS for the scores of one workgroup
-static_assert(kSelThreads == 256, "one radix bin per thread");
+static_assert(kSelThreads / 64 >= kSelRows, "one wave per selected row");
 constexpr int kMaxD = 72;
 constexpr int kPoolRows = 64;                      // largest block
 
@@ -104,28 +104,16 @@ __device__ __forceinline__ uint32_t order_key(float x) {
     return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
 }
 
-// Exclusive prefix sum of v over the workgroup's kSelThreads lanes (thread
-// order); *total receives the sum.  Two barriers; every thread must call it.
-__device__ __forceinline__ int group_excl_scan(int v, int* wsum, int* total) {
-    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-    int x = v;
-#pragma unroll
-    for (int d = 1; d < 64; d <<= 1) {
-        const int y = __shfl_up(x, d, 64);
-        if (lane >= d) x += y;
-    }
-    if (lane == 63) wsum[w] = x;
-    __syncthreads();
-    int off = 0, tot = 0;
-#pragma unroll
-    for (int i = 0; i < kSelThreads / 64; ++i) {
-        const int sw = wsum[i];
-        off += i < w ? sw : 0;
-        tot += sw;
-    }
-    __syncthreads();  // wsum may be reused
-    *total = tot;
-    return off + x - v;
+// Number of lanes below this one whose bit is set in the wave mask m.
+__device__ __forceinline__ int lanes_below(unsigned long long m) {
+    return (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+}
+
+// Orders the wave's LDS accesses before and after this point (one wave only:
+// LDS executes a wave's instructions in issue order).
+__device__ __forceinline__ void wave_lds_sync() {
+    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+    __builtin_amdgcn_wave_barrier();
 }
 
 __global__ __launch_bounds__(kSelThreads) void select_kernel(const float* __restrict__ qsum,
@@ -134,16 +122,16 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(const float* __rest
                                                              int32_t* __restrict__ col_idx) {
     // scores of the workgroup's rows: rows x n_blk floats of dynamic LDS
     extern __shared__ float sc[];
-    __shared__ float qv[kSelRows][kMaxD];  // pooled queries of the rows
-    // one chunk of key means, rows padded by one float so that the lanes of a
-    // wave, reading one head dim of 64 consecutive key blocks, hit 64 banks
-    __shared__ float km[kSelChunk * (kMaxD + 1)];
+    __shared__ __attribute__((aligned(16))) float qv[kSelRows][kMaxD];  // pooled queries of the rows
+    // one chunk of key means, rows padded by four floats so that the 16-byte
+    // reads of 16 lanes (16 consecutive key blocks) cover the 64 banks once
+    __shared__ __attribute__((aligned(16))) float km[kSelChunk * (kMaxD + 4)];
     const int n_grp = (n_blk + rows - 1) / rows;
     const int bh = blockIdx.x / n_grp;
     const int qb0 = (blockIdx.x - bh * n_grp) * rows;
     const int tid = threadIdx.x;
     const int kk = keep < n_blk ? keep : n_blk;
-    const int kst = D + 1;  // LDS row stride of km
+    const int kst = D + 4;  // LDS row stride of km (floats; a multiple of 4)
     for (int i = tid; i < rows * D; i += kSelThreads) {
         const int r = i / D, d = i - r * D;
         qv[r][d] = qb0 + r < n_blk ? qsum[((size_t)bh * n_blk + qb0 + r) * D + d] : 0.0f;
@@ -151,121 +139,136 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(const float* __rest
     const float* kh = kmean + (size_t)bh * n_blk * D;
     const int pr = tid / kSelChunk;  // the pair this lane scores: row pr,
     const int pc = tid - pr * kSelChunk;  // key block c0 + pc
+    // A chunk's nc * D floats are contiguous in HBM: 16-byte pieces i, piece
+    // tid + kSelThreads j in register pf[j].  The next chunk's loads are in
+    // flight while the current one is scored.
+    constexpr int kPieces = (kSelChunk * kMaxD / 4 + kSelThreads - 1) / kSelThreads;
+    u32x4 pf[kPieces];
+    auto load_chunk = [&](int c0) {
+        const int nc = n_blk - c0 < kSelChunk ? n_blk - c0 : kSelChunk;
+        const int n16 = nc * D / 4;
+        const u32x4* src = reinterpret_cast<const u32x4*>(kh + (size_t)c0 * D);
+#pragma unroll
+        for (int j = 0; j < kPieces; ++j) {
+            const int i = tid + kSelThreads * j;
+            if (i < n16) pf[j] = src[i];
+        }
+    };
+    load_chunk(0);
     for (int c0 = 0; c0 < n_blk; c0 += kSelChunk) {
         const int nc = n_blk - c0 < kSelChunk ? n_blk - c0 : kSelChunk;
         __syncthreads();  // the previous chunk's scores are done (and qv is in)
-        // the chunk's nc * D floats are contiguous in HBM: 16-byte loads
         const int n16 = nc * D / 4;
-        const u32x4* src = reinterpret_cast<const u32x4*>(kh + (size_t)c0 * D);
-        for (int i = tid; i < n16; i += kSelThreads) {
-            const u32x4 v = src[i];
-            const int e = 4 * i, r = e / D, d = e - r * D;  // D is a multiple of 4
-            float* dst = km + r * kst + d;
-            dst[0] = __uint_as_float(v[0]);
-            dst[1] = __uint_as_float(v[1]);
-            dst[2] = __uint_as_float(v[2]);
-            dst[3] = __uint_as_float(v[3]);
+#pragma unroll
+        for (int j = 0; j < kPieces; ++j) {
+            const int i = tid + kSelThreads * j;
+            if (i < n16) {
+                const int e = 4 * i, r = e / D, d = e - r * D;  // D is a multiple of 4
+                *reinterpret_cast<u32x4*>(km + r * kst + d) = pf[j];
+            }
         }
         __syncthreads();
+        if (c0 + kSelChunk < n_blk) load_chunk(c0 + kSelChunk);
         if (pr < rows && pc < nc) {
-            const float* kv = km + pc * kst;
+            const u32x4* kv = reinterpret_cast<const u32x4*>(km + pc * kst);
+            const u32x4* qq = reinterpret_cast<const u32x4*>(qv[pr]);
             float s = 0.0f;
-            for (int d = 0; d < D; ++d) s = __fadd_rn(s, __fmul_rn(qv[pr][d], kv[d]));
+            for (int d4 = 0; d4 < D / 4; ++d4) {
+                const u32x4 a = qq[d4], b = kv[d4];
+#pragma unroll
+                for (int e = 0; e < 4; ++e) s = __fadd_rn(s, __fmul_rn(__uint_as_float(a[e]), __uint_as_float(b[e])));
+            }
             sc[pr * n_blk + c0 + pc] = s;
         }
     }
     __syncthreads();
-    // Selection, row by row.  Each thread owns a contiguous run of at most 16
-    // candidate blocks.  The keep - 1 best blocks other than the diagonal are
-    // found by radix selection on the 32-bit keys: four passes of 8-bit digits,
-    // from the top, narrow the key of the (keep-1)-th best block (the
-    // threshold) and how many blocks holding exactly that key are kept; those
-    // go to the lowest indices.  Every block with a larger key is kept.
-    __shared__ int hist[256];
-    __shared__ int wsum[kSelThreads / 64];
-    __shared__ int pick[2];
-    const int seg = (n_blk + kSelThreads - 1) / kSelThreads;
-    const int c_lo = tid * seg < n_blk ? tid * seg : n_blk;
-    const int c_hi = c_lo + seg < n_blk ? c_lo + seg : n_blk;
+    // Selection: wave w takes row w.  Candidate block c = lane + 64 i (round
+    // i).  The keep - 1 best blocks other than the diagonal are found by radix
+    // selection on the 32-bit keys: four passes of 8-bit digits, from the top,
+    // narrow the key of the (keep-1)-th best block (the threshold) and how many
+    // blocks holding exactly that key are kept; those go to the lowest indices.
+    // Every block with a larger key is kept.
+    __shared__ int hist[kSelThreads / 64][256];
+    const int lane = tid & 63, w = tid >> 6;
+    const int qb = qb0 + w;
+    if (w >= rows || qb >= n_blk) return;  // no barrier follows
+    const float* row = sc + w * n_blk;
+    int* hw = hist[w];
+    const int n_round = (n_blk + 63) / 64;
     const int need = kk - 1;  // other blocks to keep, < n_blk
-    for (int r = 0; r < rows; ++r) {
-        const int qb = qb0 + r;
-        if (qb >= n_blk) break;  // uniform over the workgroup
-        const float* row = sc + r * n_blk;
-        uint32_t key[16];
+    uint32_t thr = 0, thr_mask = 0;  // digits of the threshold found so far
+    int rem = need;                   // blocks still to keep at the threshold
+    if (need > 0 && need < n_blk - 1) {
+        for (int shift = 24; shift >= 0; shift -= 8) {
 #pragma unroll
-        for (int i = 0; i < 16; ++i) key[i] = c_lo + i < c_hi ? order_key(row[c_lo + i]) : 0u;
-        uint32_t thr = 0, thr_mask = 0;  // digits of the threshold found so far
-        int rem = need;                   // blocks still to keep at the threshold
-        if (need > 0 && need < n_blk - 1) {
-            for (int shift = 24; shift >= 0; shift -= 8) {
-                hist[tid] = 0;  // kSelThreads == 256 bins
-                __syncthreads();
-#pragma unroll
-                for (int i = 0; i < 16; ++i) {
-                    const int c = c_lo + i;
-                    if (c < c_hi && c != qb && (key[i] & thr_mask) == thr) atomicAdd(&hist[(key[i] >> shift) & 255u], 1);
+            for (int j = 0; j < 4; ++j) hw[4 * lane + j] = 0;
+            wave_lds_sync();
+            for (int i = 0; i < n_round; ++i) {
+                const int c = lane + 64 * i;
+                if (c < n_blk && c != qb) {
+                    const uint32_t key = order_key(row[c]);
+                    if ((key & thr_mask) == thr) atomicAdd(&hw[(key >> shift) & 255u], 1);
                 }
-                __syncthreads();
-                // bins from the top: S(t) blocks have digit >= t; the threshold's
-                // digit is the t with S(t+1) < rem <= S(t)
-                const int h = hist[tid];
-                int tot;
-                const int below = group_excl_scan(h, wsum, &tot);
-                const int s_t = tot - below;
-                if (h > 0 && s_t >= rem && s_t - h < rem) {
-                    pick[0] = tid;
-                    pick[1] = rem - (s_t - h);
-                }
-                __syncthreads();
-                thr |= (uint32_t)pick[0] << shift;
-                thr_mask |= 255u << shift;
-                rem = pick[1];
             }
+            wave_lds_sync();
+            // lane L holds bins 4L .. 4L+3; S(t) counts the blocks with digit >= t
+            // and the threshold's digit is the t with S(t+1) < rem <= S(t)
+            int h[4], sum = 0;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                h[j] = hw[4 * lane + j];
+                sum += h[j];
+            }
+            int incl = sum;  // inclusive sum over lanes 0 .. lane
+#pragma unroll
+            for (int d = 1; d < 64; d <<= 1) {
+                const int y = __shfl_up(incl, d, 64);
+                if (lane >= d) incl += y;
+            }
+            const int tot = __shfl(incl, 63, 64);
+            int s_t = tot - incl;  // bins above this lane's four
+            int dig = -1, nrem = 0;
+#pragma unroll
+            for (int j = 3; j >= 0; --j) {
+                s_t += h[j];
+                if (h[j] > 0 && s_t >= rem && s_t - h[j] < rem) {
+                    dig = 4 * lane + j;
+                    nrem = rem - (s_t - h[j]);
+                }
+            }
+            const unsigned long long found = __ballot(dig >= 0);
+            const int src = __builtin_ctzll(found);  // exactly one lane finds it
+            thr |= (uint32_t)__shfl(dig, src, 64) << shift;
+            thr_mask |= 255u << shift;
+            rem = __shfl(nrem, src, 64);
         }
-        // ties at the threshold in ascending block order: this thread's first
-        // tie is number `tie0` among them
-        int n_tie = 0;
-#pragma unroll
-        for (int i = 0; i < 16; ++i) n_tie += (c_lo + i < c_hi && c_lo + i != qb && key[i] == thr) ? 1 : 0;
-        int tot_tie;
-        int tie = group_excl_scan(n_tie, wsum, &tot_tie);
-        unsigned kept_bits = 0;  // bit i: candidate c_lo + i is kept
-        int n_kept = 0;
-#pragma unroll
-        for (int i = 0; i < 16; ++i) {
-            const int c = c_lo + i;
-            if (c >= c_hi) continue;
-            bool kept;
+    }
+    // kept blocks in ascending order, ties at the threshold to the lowest indices
+    const size_t row_off = ((size_t)bh * n_blk + qb) * kk;
+    int n_tie = 0, n_out = 0;
+    for (int i = 0; i < n_round; ++i) {
+        const int c = lane + 64 * i;
+        bool kept = false, tie = false;
+        if (c < n_blk) {
             if (c == qb || need >= n_blk - 1) {
                 kept = true;
-            } else if (need == 0) {
-                kept = false;
-            } else if (key[i] == thr) {
-                kept = tie < rem;
-                ++tie;
-            } else {
-                kept = key[i] > thr;
-            }
-            if (kept) {
-                kept_bits |= 1u << i;
-                ++n_kept;
+            } else if (need > 0) {
+                const uint32_t key = order_key(row[c]);
+                tie = key == thr;
+                kept = key > thr;
             }
         }
-        int tot_kept;
-        int pos = group_excl_scan(n_kept, wsum, &tot_kept);  // == kk (total order)
-        const size_t row_off = ((size_t)bh * n_blk + qb) * kk;
-#pragma unroll
-        for (int i = 0; i < 16; ++i) {
-            if ((kept_bits >> i) & 1u) {
-                if (pos < kk) col_idx[row_off + pos] = c_lo + i;
-                ++pos;
-            }
-        }
-        if (tid == 0) {
-            row_ptr[(size_t)bh * (n_blk + 1) + qb] = (int32_t)row_off;
-            if (qb == n_blk - 1) row_ptr[(size_t)bh * (n_blk + 1) + n_blk] = (int32_t)(row_off + kk);
-        }
+        const unsigned long long tm = __ballot(tie);
+        if (tie) kept = n_tie + lanes_below(tm) < rem;
+        n_tie += __popcll(tm);
+        const unsigned long long km_ = __ballot(kept);
+        const int pos = n_out + lanes_below(km_);
+        if (kept && pos < kk) col_idx[row_off + pos] = c;  // exactly kk kept (total order)
+        n_out += __popcll(km_);
+    }
+    if (lane == 0) {
+        row_ptr[(size_t)bh * (n_blk + 1) + qb] = (int32_t)row_off;
+        if (qb == n_blk - 1) row_ptr[(size_t)bh * (n_blk + 1) + n_blk] = (int32_t)(row_off + kk);
     }
 }
 
