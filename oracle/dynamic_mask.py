@@ -21,7 +21,9 @@ and query block qb:
     and Eq.2's 1/sqrt(d_h)) do not change its ranking and are left out;
   * query block qb keeps its own block (so S_i is never empty, as Eq.5
     requires) and the keep - 1 highest-scoring other blocks, a tie going to the
-    lower index; the row is stored in ascending block order.
+    lower index; the row is stored in ascending block order;
+  * a NaN score (non-finite inputs) ranks as -inf: after every other score,
+    and tied with -inf, so the lower index goes first.
 
 Because the choice is an integer decision taken from floating-point scores, the
 arithmetic above is fixed operation by operation, and the GPU builder performs
@@ -82,7 +84,8 @@ def select(scores, keep):
     col_idx = np.empty(nb * kk, dtype=np.int64)
     for qb in range(nb):
         others = [kb for kb in range(nb) if kb != qb]
-        others.sort(key=lambda kb: (-float(scores[qb, kb]), kb))
+        rank_score = lambda kb: -np.inf if np.isnan(scores[qb, kb]) else float(scores[qb, kb])
+        others.sort(key=lambda kb: (-rank_score(kb), kb))
         row = sorted([qb] + others[:kk - 1])
         col_idx[qb * kk:(qb + 1) * kk] = row
     return row_ptr.astype(np.int32), col_idx.astype(np.int32)

@@ -127,3 +127,26 @@ def test_attention_over_dynamic_masks(gpu, shape):
             assert_stat_close(to_np(m_s)[sl], Ms2, f"{what} m_s", floor=1.0)
             assert_stat_close(to_np(l_s)[sl], Ls2, f"{what} l_s")
             assert_bf16_close(to_np(out)[sl], oa.reshape(Os2, Rho, R, 0.0), f"{what} fused")
+
+
+def test_non_finite_scores_follow_the_oracle(gpu):
+    # +inf and -inf in one key block make its mean NaN, so every score against
+    # it is NaN (ranked as -inf); +inf alone in another block gives +-inf scores
+    import torch
+
+    B, H, T, D, bs = 1, 2, 8 * 64, 64, 64
+    print("[dynamic] non-finite scores", flush=True)
+    rng = np.random.default_rng(11)
+    q = rng.standard_normal((B, H, T, D)).astype(np.float32)
+    k = rng.standard_normal((B, H, T, D)).astype(np.float32)
+    k[:, :, 3 * bs, 5] = np.inf
+    k[:, :, 3 * bs + 1, 5] = -np.inf
+    k[:, 1, 6 * bs + 2, 7] = np.inf
+    qb_, kb_ = synth.f32_to_bf16_bits(q), synth.f32_to_bf16_bits(k)
+    mask = rt.dynamic_index(to_dev(qb_), to_dev(kb_), bs, 3)
+    torch.cuda.synchronize()
+    rp, ci = _mask_np(mask)
+    with np.errstate(invalid="ignore", over="ignore"):
+        orp, oci = dm.dynamic_mask(synth.bf16_bits_to_f32(qb_), synth.bf16_bits_to_f32(kb_), bs, 3)
+    assert np.array_equal(rp, orp)
+    assert np.array_equal(ci, oci)

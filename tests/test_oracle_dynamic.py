@@ -151,3 +151,18 @@ def test_mutants_are_caught(monkeypatch, mutant):
         monkeypatch.setattr(dm, "select", _select_no_diagonal)
         with pytest.raises(AssertionError):
             test_keep_extremes()
+
+
+def test_nan_scores_rank_last_and_tie_with_minus_inf():
+    # reading: a NaN score counts as -inf, so it follows every finite score and
+    # ties with -inf, broken by the lower index
+    nan, inf = np.float32(np.nan), np.float32(np.inf)
+    s = np.zeros((6, 6), dtype=np.float32)
+    s[0] = [5.0, nan, -inf, 1.0, nan, -2.0]
+    rp, ci = dm.select(s, keep=4)
+    assert list(ci[rp[0]:rp[1]]) == [0, 1, 3, 5]  # 1, -2, then the first of {nan@1, -inf@2, nan@4}
+    rp, ci = dm.select(s, keep=5)
+    assert list(ci[rp[0]:rp[1]]) == [0, 1, 2, 3, 5]
+    s[0] = [0.0, nan, nan, nan, nan, nan]
+    rp, ci = dm.select(s, keep=3)
+    assert list(ci[rp[0]:rp[1]]) == [0, 1, 2]
