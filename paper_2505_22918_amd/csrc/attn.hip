@@ -132,7 +132,9 @@ __device__ __forceinline__ void wait_vm() {
 
 // 16 bytes per lane from buffer `rsrc` at byte offset `voff` into LDS at
 // m0 + 16 * lane (buffer_load_dwordx4 ... lds).  m0 is reserved by the compiler
-// (never allocated) and is set before every use.  Issued from inline assembly so
+// (never allocated) and is set before every use; this is sound only while the
+// compiled code keeps nothing else in m0, which the tests check on the
+// assembly of every build.  Issued from inline assembly so
 // the compiler neither orders these loads against LDS reads of other stages nor
 // waits for them; the kernel waits on the vector-memory counter itself.
 __device__ __forceinline__ void dma16(uint32_t lds_addr, int voff, i32x4 rsrc) {
