@@ -156,7 +156,8 @@ rt_status rt_index_build(const rt_pattern* pattern, int32_t T, int32_t block, in
  * product accumulates in fp32 over ascending d, product and sum each rounded
  * (no fused multiply-add).  qb keeps itself (Eq.5 needs a non-empty kept set)
  * and the keep - 1 best other blocks (higher score first, ties to the lower
- * index, a NaN score last), stored ascending, so every row holds exactly
+ * index; a NaN score ranks as -inf, after every other score), stored
+ * ascending, so every row holds exactly
  * kk = min(keep, n_qblk) blocks.  The result is one mask per (batch, head):
  * row_ptr [B*H][n_qblk + 1] (absolute offsets, row (bh, qb) starting at
  * (bh*n_qblk + qb)*kk) and col_idx [B*H*n_qblk*kk], for an rt_bsr with
