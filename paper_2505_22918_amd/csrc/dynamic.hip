@@ -21,8 +21,8 @@
 //                  128 + d does the same for K and divides by the token count.
 //                  Writes qsum and kmean [B*H][n_blk][D].
 //   select_kernel  one workgroup per (batch, head) and `rows` consecutive
-//                  query blocks (4, or 2 above 2048 blocks, so that the
-//                  scores fit 32 KB of LDS): the key means pass through LDS in chunks of
+//                  query blocks (8, halved until the scores fit 32 KB of
+//                  LDS: 2 at 4096 blocks): the key means pass through LDS in chunks of
 //                  kSelChunk blocks (one 16-byte load per lane and round), each
 //                  lane scoring one (query block, key block) pair of the chunk;
 //                  then one wave per row: a radix selection of the keep - 1
@@ -44,8 +44,8 @@ namespace rt {
 namespace {
 
 constexpr int kPoolThreads = 256;
-constexpr int kSelThreads = 256;
-constexpr int kSelRows = 4;                         // most query blocks per select workgroup
+constexpr int kSelThreads = 512;
+constexpr int kSelRows = 8;                         // most query blocks per select workgroup
 constexpr int kSelChunk = kSelThreads / kSelRows;  // key blocks per LDS chunk
 constexpr int kSelScoreBytes = 32 << 10;           // LDS for the scores of one workgroup
 static_assert(kSelThreads / 64 >= kSelRows, "one wave per selected row");
