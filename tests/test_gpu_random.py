@@ -5,8 +5,10 @@ width 64 or 72, block 32 or 64), a mask layout (one shared mask, one per head,
 one per (batch, head)) and random explicit masks with rows of one to every key
 block, then checks sparse attention with and without statistics, the fused
 reshape (Eq.9 with a ramp, Eq.10), dense attention with statistics (Eq.1,
-Eq.4), the one-pass caching step (Eq.8, Eq.10) and post-softmax masking (Eq.7)
-element by element.
+Eq.4), the one-pass caching step (Eq.8, Eq.10), post-softmax masking (Eq.7),
+the ablation without the statistical reshape (NULL rho), and a dynamic block
+mask built from the case's Q and K (CSR bit for bit, then the fused call over
+it) element by element.
 """
 
 import os
@@ -17,6 +19,7 @@ import pytest
 import paper_2505_22918_amd as rt
 from oracle import attention as oa
 from oracle import block_index as ob
+from oracle import dynamic_mask as dm
 from paper_2505_22918_amd import synth
 
 from parity import assert_bf16_close, assert_stat_close, to_dev, to_np
@@ -79,7 +82,18 @@ def test_random_configuration(gpu, i):
     of, mf, lf = rt.attn_full(q, k, v, block=block)
     oc, rhoc, rc, mc, lc = rt.attn_cache(q, k, v, mask)
     op = rt.attn_postmask(q, k, v, mask)
+    # the ablation without the statistical reshape: R' = O_full - O_s, then O_s + R
+    onr, rho_none, rnr = rt.attn_cache(q, k, v, mask, stats=False, ratio=False)
+    o_nr = rt.attn_sparse_reshape(q, k, v, mask, None, resid, rho_delta=delta)
+    # a dynamic mask from this case's Q and K, and the fused call over it
+    keep = int(rng.integers(1, nb + 2))
+    dmask = rt.dynamic_index(q, k, block, keep)
+    o_dyn = rt.attn_sparse_reshape(q, k, v, dmask, rho, resid, rho_delta=delta)
     torch.cuda.synchronize()
+    assert rho_none is None
+    drp, dci = dm.dynamic_mask(synth.bf16_bits_to_f32(s[0]), synth.bf16_bits_to_f32(s[1]), block, keep)
+    assert np.array_equal(dmask.row_ptr.cpu().numpy(), drp), f"case {i} dynamic row_ptr"
+    assert np.array_equal(dmask.col_idx.cpu().numpy(), dci), f"case {i} dynamic col_idx"
 
     Q, K, V = (synth.bf16_bits_to_f32(x).astype(np.float64) for x in s)
     Of, Mf, Lf = oa.full_attention(Q, K, V)
@@ -88,7 +102,8 @@ def test_random_configuration(gpu, i):
     assert_stat_close(to_np(lf), Lf, f"case {i} l_full")
     rho_h, resid_h = to_np(rho), to_np(resid)
     got = {n: to_np(t) for n, t in dict(o_st=o_st, m_st=m_st, l_st=l_st, o_ns=o_ns, o_fu=o_fu, oc=oc, rhoc=rhoc,
-                                         rc=rc, mc=mc, lc=lc, op=op).items()}
+                                         rc=rc, mc=mc, lc=lc, op=op, onr=onr, rnr=rnr, o_nr=o_nr,
+                                         o_dyn=o_dyn).items()}
     for b in range(B):
         for h in range(H):
             mid = 0 if n_masks == 1 else (h if n_masks == H else b * H + h)
@@ -109,6 +124,14 @@ def test_random_configuration(gpu, i):
             assert_stat_close(got["mc"][sl], Mf[sl], f"{tag} caching m", floor=1.0)
             assert_stat_close(got["lc"][sl], Lf[sl], f"{tag} caching l")
             assert_bf16_close(got["op"][sl], Rho[..., None] * Os, f"{tag} (A o M) V")
+            assert_bf16_close(got["onr"][sl], Of[sl], f"{tag} ratio-free caching O_full")
+            assert_bf16_close(got["rnr"][sl], oa.residual_no_ratio(Of[sl], Os), f"{tag} ratio-free R'")
+            assert_bf16_close(got["o_nr"][sl], oa.add_residual(Os, resid_h[sl]), f"{tag} ratio-free fused")
+            m = b * H + h
+            hrp = drp[m * (nb + 1):(m + 1) * (nb + 1)]
+            Od, _, _ = oa.sparse_attention(Q[sl], K[sl], V[sl], hrp - hrp[0], dci[hrp[0]:hrp[-1]], block)
+            assert_bf16_close(got["o_dyn"][sl], oa.reshape(Od, rho_h[sl], resid_h[sl], delta),
+                              f"{tag} fused over the dynamic mask")
 
 
 # Long rows: 40 to 150 kept blocks, so walks cross the 64-chunk table refill and,
