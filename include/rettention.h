@@ -35,6 +35,9 @@
  *    the same call (RT_EINVAL): every work item reads all of a head's K and V
  *    while others write their output rows.
  *  - A call with B*H*T == 0 checks its arguments and enqueues nothing.
+ *  - Every call launches on the calling thread's current HIP device (and the
+ *    allocation-free build uses that device's copy of its workspace): the
+ *    device pointers and the stream must belong to it.
  */
 #ifndef RETTENTION_H
 #define RETTENTION_H

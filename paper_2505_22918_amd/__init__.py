@@ -67,6 +67,42 @@ def _stream(t):
     return torch.cuda.current_stream(t.device).cuda_stream
 
 
+_GETDEV = None
+
+
+def _current_device():
+    """Index of the current device (torch's raw getter: no lazy-init check)."""
+    global _GETDEV
+    if _GETDEV is None:
+        torch = _torch()
+        _GETDEV = getattr(torch._C, "_cuda_getDevice", None) or torch.cuda.current_device
+    return _GETDEV()
+
+
+class _on(object):
+    """Makes the device of tensor t the current device while the library is
+    called (the library launches on the current device and looks up its
+    per-device state there), and restores the previous one afterwards."""
+
+    __slots__ = ("idx", "prev")
+
+    def __init__(self, t):
+        self.idx = t.get_device()
+        self.prev = -1
+
+    def __enter__(self):
+        cur = _current_device()
+        if cur != self.idx:
+            self.prev = cur
+            _torch().cuda.set_device(self.idx)
+        return self
+
+    def __exit__(self, *exc):
+        if self.prev >= 0:
+            _torch().cuda.set_device(self.prev)
+        return False
+
+
 def _ptr(t):
     """Device address of t, or NULL for None (ctypes takes ints for void*)."""
     return t.data_ptr() if t is not None else None
@@ -215,8 +251,9 @@ def build_index(T, block, kind, device="cuda", host_mask=None, **pat) -> BlockMa
     row_ptr = torch.empty(n_masks * (n_blk + 1), dtype=torch.int32, device=device)
     col_idx = torch.empty(max(nnz, 1), dtype=torch.int32, device=device)
     p = _pattern(kind, mask=dmask, host_mask=hm, n_masks=n_masks, **pat)
-    _lib.check("rt_index_build", lib.rt_index_build(ctypes.byref(p), int(T), int(block), _ptr(row_ptr),
-                                                    _ptr(col_idx), int(nnz), _stream(row_ptr)))
+    with _on(row_ptr):
+        _lib.check("rt_index_build", lib.rt_index_build(ctypes.byref(p), int(T), int(block), _ptr(row_ptr),
+                                                        _ptr(col_idx), int(nnz), _stream(row_ptr)))
     if dmask is not None:
         # keep the mask alive until the build has run on the stream
         torch.cuda.current_stream(row_ptr.device).synchronize()
@@ -241,9 +278,10 @@ def dynamic_index(q, k, block, keep) -> BlockMask:
     row_ptr = torch.empty(B * H * (n_blk + 1), dtype=torch.int32, device=q.device)
     col_idx = torch.empty(max(nnz, 1), dtype=torch.int32, device=q.device)
     work = torch.empty(max(int(ws.value) // 4, 4), dtype=torch.float32, device=q.device)
-    _lib.check("rt_dynamic_index", lib.rt_dynamic_index(_ptr(q), _ptr(k), dims, int(block), int(keep), _ptr(row_ptr),
-                                                        _ptr(col_idx), int(nnz), _ptr(work), int(ws.value),
-                                                        _stream(q)))
+    with _on(q):
+        _lib.check("rt_dynamic_index", lib.rt_dynamic_index(_ptr(q), _ptr(k), dims, int(block), int(keep),
+                                                            _ptr(row_ptr), _ptr(col_idx), int(nnz), _ptr(work),
+                                                            int(ws.value), _stream(q)))
     # `work` returns to torch's stream-ordered cache here; a later reuse on this
     # stream runs after the launch that reads it
     return BlockMask(row_ptr, col_idx[:nnz], int(block), n_blk, int(nnz), B * H)
@@ -259,8 +297,9 @@ def attn_full(q, k, v, block=64, stats=True, out=None):
     if stats:
         m = torch.empty(q.shape[:3], dtype=torch.float32, device=q.device)
         l = torch.empty_like(m)
-    _lib.check("rt_attn_full", lib.rt_attn_full(_ptr(q), _ptr(k), _ptr(v), dims, int(block), _ptr(o),
-                                                _ptr(m), _ptr(l), _stream(q)))
+    with _on(q):
+        _lib.check("rt_attn_full", lib.rt_attn_full(_ptr(q), _ptr(k), _ptr(v), dims, int(block), _ptr(o),
+                                                    _ptr(m), _ptr(l), _stream(q)))
     return (o, m, l) if stats else o
 
 
@@ -276,8 +315,9 @@ def attn_sparse(q, k, v, mask: BlockMask, stats=True, out=None):
         m = torch.empty(q.shape[:3], dtype=torch.float32, device=q.device)
         l = torch.empty_like(m)
     bsr = mask.c_struct()
-    _lib.check("rt_attn_sparse", lib.rt_attn_sparse(_ptr(q), _ptr(k), _ptr(v), dims, ctypes.byref(bsr),
-                                                    _ptr(o), _ptr(m), _ptr(l), _stream(q)))
+    with _on(q):
+        _lib.check("rt_attn_sparse", lib.rt_attn_sparse(_ptr(q), _ptr(k), _ptr(v), dims, ctypes.byref(bsr),
+                                                        _ptr(o), _ptr(m), _ptr(l), _stream(q)))
     return (o, m, l) if stats else o
 
 
@@ -298,8 +338,9 @@ def attn_cache(q, k, v, mask: BlockMask, stats=True, out=None, ratio=True):
         m = torch.empty(q.shape[:3], dtype=torch.float32, device=q.device)
         l = torch.empty_like(m)
     bsr = mask.c_struct()
-    _lib.check("rt_attn_cache", lib.rt_attn_cache(_ptr(q), _ptr(k), _ptr(v), dims, ctypes.byref(bsr), _ptr(o),
-                                                  _ptr(m), _ptr(l), _ptr(rho), _ptr(resid), _stream(q)))
+    with _on(q):
+        _lib.check("rt_attn_cache", lib.rt_attn_cache(_ptr(q), _ptr(k), _ptr(v), dims, ctypes.byref(bsr), _ptr(o),
+                                                      _ptr(m), _ptr(l), _ptr(rho), _ptr(resid), _stream(q)))
     return (o, rho, resid, m, l) if stats else (o, rho, resid)
 
 
@@ -311,8 +352,9 @@ def attn_postmask(q, k, v, mask: BlockMask, out=None):
     _mask_on(mask, q.device)
     o = _out(out, q)
     bsr = mask.c_struct()
-    _lib.check("rt_attn_postmask", lib.rt_attn_postmask(_ptr(q), _ptr(k), _ptr(v), dims, ctypes.byref(bsr),
-                                                        _ptr(o), _stream(q)))
+    with _on(q):
+        _lib.check("rt_attn_postmask", lib.rt_attn_postmask(_ptr(q), _ptr(k), _ptr(v), dims, ctypes.byref(bsr),
+                                                            _ptr(o), _stream(q)))
     return o
 
 
@@ -336,9 +378,10 @@ def cache_build(o_full, m_full, l_full, o_sparse, m_sparse, l_sparse, ratio=True
         m_full = l_full = m_sparse = l_sparse = None
     rho = torch.empty((B, H, T), dtype=torch.float32, device=o_full.device) if ratio else None
     resid = torch.empty_like(o_full)
-    _lib.check("rt_cache_build", lib.rt_cache_build(_ptr(o_full), _ptr(m_full), _ptr(l_full), _ptr(o_sparse),
-                                                    _ptr(m_sparse), _ptr(l_sparse), _lib.RtDims(B, H, T, D),
-                                                    _ptr(rho), _ptr(resid), _stream(o_full)))
+    with _on(o_full):
+        _lib.check("rt_cache_build", lib.rt_cache_build(_ptr(o_full), _ptr(m_full), _ptr(l_full), _ptr(o_sparse),
+                                                        _ptr(m_sparse), _ptr(l_sparse), _lib.RtDims(B, H, T, D),
+                                                        _ptr(rho), _ptr(resid), _stream(o_full)))
     return rho, resid
 
 
@@ -358,9 +401,10 @@ def attn_sparse_reshape(q, k, v, mask: BlockMask, rho, resid, rho_delta=0.0, sta
         m = torch.empty(q.shape[:3], dtype=torch.float32, device=q.device)
         l = torch.empty_like(m)
     bsr = mask.c_struct()
-    _lib.check("rt_attn_sparse_reshape",
-               lib.rt_attn_sparse_reshape(_ptr(q), _ptr(k), _ptr(v), dims, ctypes.byref(bsr), _ptr(rho),
-                                          _ptr(resid), float(rho_delta), _ptr(o), _ptr(m), _ptr(l), _stream(q)))
+    with _on(q):
+        _lib.check("rt_attn_sparse_reshape",
+                   lib.rt_attn_sparse_reshape(_ptr(q), _ptr(k), _ptr(v), dims, ctypes.byref(bsr), _ptr(rho),
+                                              _ptr(resid), float(rho_delta), _ptr(o), _ptr(m), _ptr(l), _stream(q)))
     return (o, m, l) if stats else o
 
 
@@ -379,8 +423,9 @@ def reshape_apply(o_sparse, rho, resid, rho_delta=0.0, out=None):
     if rho is not None:
         _stat(rho, (B, H, T), "rho", dev)
     o = _out(out, o_sparse)
-    _lib.check("rt_reshape_apply", lib.rt_reshape_apply(_ptr(o_sparse), _ptr(rho), _ptr(resid), float(rho_delta),
-                                                        _lib.RtDims(B, H, T, D), _ptr(o), _stream(o_sparse)))
+    with _on(o_sparse):
+        _lib.check("rt_reshape_apply", lib.rt_reshape_apply(_ptr(o_sparse), _ptr(rho), _ptr(resid), float(rho_delta),
+                                                            _lib.RtDims(B, H, T, D), _ptr(o), _stream(o_sparse)))
     return o
 
 
