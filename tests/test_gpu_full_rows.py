@@ -57,3 +57,37 @@ def test_cogvideox_every_row_of_two_heads(gpu):
         assert_bf16_close(g["out"][sl], Out, f"{what} fused")
         worst = int(np.argmax(np.abs(g["out"][sl] - Out).max(axis=-1)[0, 0]))
         print(f"[full-rows] ({b},{h}) ok, worst fused row {worst}", flush=True)
+
+
+def test_pixart_sigma_2k_every_row_of_one_head(gpu):
+    # the 72-wide kernel (80-wide Q K^T, 96-row O^T) on a whole head at full size
+    import torch
+
+    wl = synth.WORKLOADS["pixart_sigma_2k"]
+    b, h = 1, 7
+    print(f"[full-rows] pixart_sigma_2k T={wl.T} D={wl.D} pair=({b},{h})", flush=True)
+    s1 = synth.make_qkv(wl, 1)
+    s2 = synth.make_qkv(wl, 2)
+    orp, oci = _oracle_csr(wl)
+    mask = _gpu_mask(wl)
+    q1, k1, v1 = (to_dev(x) for x in s1)
+    of, rho, resid = rt.attn_cache(q1, k1, v1, mask, stats=False)
+    del q1, k1, v1
+    q2, k2, v2 = (to_dev(x) for x in s2)
+    out = torch.empty_like(q2)
+    rt.attn_sparse_reshape(q2, k2, v2, mask, rho, resid, 0.0, out=out)
+    torch.cuda.synchronize()
+    sl = (slice(b, b + 1), slice(h, h + 1))
+    Q1, K1, V1 = (f64(x[sl]) for x in s1)
+    Q2, K2, V2 = (f64(x[sl]) for x in s2)
+    Of, Mf, Lf = oa.full_attention(Q1, K1, V1)
+    Os, Ms, Ls = oa.sparse_attention(Q1, K1, V1, orp, oci, wl.block)
+    Rho = oa.rho(Ms, Ls, Mf, Lf)
+    R = oa.residual(Of, Os, Rho)
+    Os2, _, _ = oa.sparse_attention(Q2, K2, V2, orp, oci, wl.block)
+    what = f"pixart_sigma_2k ({b},{h}) every row"
+    assert_bf16_close(to_np(of)[sl], Of, f"{what} O_full")
+    assert_stat_close(to_np(rho)[sl], Rho, f"{what} rho")
+    assert_bf16_close(to_np(resid)[sl], R, f"{what} R")
+    assert_bf16_close(to_np(out)[sl], oa.reshape(Os2, Rho, R, 0.0), f"{what} fused")
+

@@ -116,3 +116,51 @@ def test_calls_follow_the_current_stream(gpu):
     torch.cuda.current_stream().wait_stream(side)
     torch.cuda.synchronize()
     assert torch.equal(res, ref)
+
+
+def test_dynamic_mask_and_fused_call_replay_together(gpu):
+    import torch
+
+    print("[graph] dynamic mask, then the fused call over it", flush=True)
+    _, q, k, v = _setup(seed=6)
+    mask0 = rt.dynamic_index(q, k, 64, 3)
+    o_full, rho, resid = rt.attn_cache(q, k, v, mask0, stats=False)
+    out = torch.empty_like(q)
+    held = {}
+
+    def step():
+        m = rt.dynamic_index(q, k, 64, 3)  # its arrays come from the graph's pool
+        held["mask"] = m
+        rt.attn_sparse_reshape(q, k, v, m, rho, resid, rho_delta=0.0, out=out)
+
+    g = _capture(step)
+    for i in range(3):
+        q.mul_(-1.05)  # moves the block scores, so the kept sets change
+        out.zero_()
+        torch.cuda.synchronize()
+        e_mask = rt.dynamic_index(q, k, 64, 3)
+        e_out = rt.attn_sparse_reshape(q, k, v, e_mask, rho, resid, rho_delta=0.0)
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(held["mask"].row_ptr, e_mask.row_ptr), f"replay {i}: row_ptr"
+        assert torch.equal(held["mask"].col_idx, e_mask.col_idx), f"replay {i}: col_idx"
+        assert torch.equal(out, e_out), f"replay {i}: fused output"
+
+
+def test_repeated_calls_are_bitwise_identical(gpu):
+    # no atomics and a fixed accumulation order: the same inputs give the same bits
+    import torch
+
+    print("[determinism] repeated calls", flush=True)
+    mask, q, k, v = _setup(seed=7)
+    runs = []
+    for _ in range(3):
+        o_f, rho, resid, m, l = rt.attn_cache(q, k, v, mask)
+        dm_ = rt.dynamic_index(q, k, 64, 3)
+        out = rt.attn_sparse_reshape(q, k, v, mask, rho, resid, rho_delta=0.02)
+        dense = rt.attn_full(q, k, v, block=64, stats=False)
+        runs.append((o_f, rho, resid, m, l, dm_.col_idx, out, dense))
+    torch.cuda.synchronize()
+    for r in runs[1:]:
+        for a, b in zip(runs[0], r):
+            assert torch.equal(a, b)
