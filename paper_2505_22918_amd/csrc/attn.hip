@@ -260,6 +260,18 @@ void attn_fwd(AttnArgs a) {
     }
     // rows of this block in Q / R / O; rows past T read as zeros
     const i32x4 q_rs = buffer_rsrc(a.q + head_off + (size_t)row0 * D, nrow * D * 2);
+    // Q^T operands: lane holds query l32 of tile qt, head dims 16s + 8hi .. +7
+    // (zero past D and past T).  Issued first, so that their HBM latency runs
+    // under the reads of the CSR row below.
+    u32x4 qraw[QT][DS];
+#pragma unroll
+    for (int qt = 0; qt < QT; ++qt) {
+#pragma unroll
+        for (int s = 0; s < DS; ++s) {
+            const int ch = 2 * s + hi;
+            qraw[qt][s] = vload16(ch < DC ? (qt * 32 + l32) * (D * 2) + ch * 16 : kOob, q_rs);
+        }
+    }
 
     // ---- kept key blocks of this query block ----------------------------------------
     int e_beg, e_end;
@@ -401,17 +413,6 @@ void attn_fwd(AttnArgs a) {
     for (int qt = 0; qt < QT; ++qt) {
         const int row = row0 + qt * 32 + l32;
         rho_r[qt] = (RESHAPE && a.rho && row < T) ? a.rho[(size_t)bh * T + row] : 0.f;
-    }
-    // Q^T operands: lane holds query l32 of tile qt, head dims 16s + 8hi .. +7
-    // (zero past D and past T)
-    u32x4 qraw[QT][DS];
-#pragma unroll
-    for (int qt = 0; qt < QT; ++qt) {
-#pragma unroll
-        for (int s = 0; s < DS; ++s) {
-            const int ch = 2 * s + hi;
-            qraw[qt][s] = vload16(ch < DC ? (qt * 32 + l32) * (D * 2) + ch * 16 : kOob, q_rs);
-        }
     }
     const int c0 = first_off(0);
     const int c1 = first_off(1);
