@@ -166,3 +166,19 @@ def test_nan_scores_rank_last_and_tie_with_minus_inf():
     s[0] = [0.0, nan, nan, nan, nan, nan]
     rp, ci = dm.select(s, keep=3)
     assert list(ci[rp[0]:rp[1]]) == [0, 1, 2]
+
+
+def test_hand_derived_golden_masks():
+    import json
+    import os
+
+    path = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden", "dynamic_mask_rows.json")
+    with open(path) as f:
+        cases = json.load(f)["cases"]
+    for c in cases:
+        q = np.array(c["q"], dtype=np.float32)[None, None]
+        k = np.array(c["k"], dtype=np.float32)[None, None]
+        for keep, rows in c["rows"].items():
+            rp, ci = dm.dynamic_mask(q, k, c["block"], int(keep))
+            got = [list(ci[rp[r]:rp[r + 1]]) for r in range(len(rows))]
+            assert got == rows, (c["name"], keep, got)
