@@ -150,3 +150,32 @@ def test_non_finite_scores_follow_the_oracle(gpu):
         orp, oci = dm.dynamic_mask(synth.bf16_bits_to_f32(qb_), synth.bf16_bits_to_f32(kb_), bs, 3)
     assert np.array_equal(rp, orp)
     assert np.array_equal(ci, oci)
+
+
+def test_hand_derived_masks_on_the_gpu(gpu):
+    # tests/golden/dynamic_mask_rows.json scaled to the library's shapes: each
+    # token repeated 16 times (blocks of 2 tokens become blocks of 32; sums scale
+    # by 16 and means stay, so every ordering and tie is unchanged) and the two
+    # head dims padded with zeros to 64
+    import json
+    import os
+
+    import torch
+
+    path = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden", "dynamic_mask_rows.json")
+    with open(path) as f:
+        cases = json.load(f)["cases"]
+    for c in cases:
+        print(f"[dynamic] golden case {c['name']}", flush=True)
+        T = 16 * c["T"]
+        q = np.zeros((1, 1, T, 64), np.float32)
+        k = np.zeros((1, 1, T, 64), np.float32)
+        q[0, 0, :, :2] = np.repeat(np.array(c["q"], np.float32), 16, axis=0)
+        k[0, 0, :, :2] = np.repeat(np.array(c["k"], np.float32), 16, axis=0)
+        qd, kd = to_dev(synth.f32_to_bf16_bits(q)), to_dev(synth.f32_to_bf16_bits(k))
+        for keep, rows in c["rows"].items():
+            mask = rt.dynamic_index(qd, kd, 16 * c["block"], int(keep))
+            torch.cuda.synchronize()
+            rp, ci = _mask_np(mask)
+            got = [list(ci[rp[r]:rp[r + 1]]) for r in range(len(rows))]
+            assert got == rows, (c["name"], keep, got)
